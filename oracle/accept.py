@@ -1,0 +1,190 @@
+"""fp64 oracle of speculative acceptance and the final sample (test infrastructure).
+
+Notation: p is the TARGET model's distribution, q the DRAFT (small
+speculative model's) distribution.  The paper's Eq. (1) uses the opposite
+letters (its p is the SSM's, its q the LLM's) and accepts a candidate with
+probability min(1, target/draft); only the letters differ.
+
+Chain (Sec. 2.2, Eq. (1); Sec. 4.3 for the extra token), per request with k
+drafts x_1..x_k and k+1 target rows:
+
+  p_j = softmax(target_logits[row j])              j = 0..k   (row j scores x_{j+1})
+  q_j = draft_probs[row j] as stored               j = 0..k-1
+  draft j is accepted iff u_j * q_j(x) < p_j(x)    (= u_j < min(1, p/q) for q > 0, u < 1)
+  a = index of the first rejection, or k if none
+  w = max(0, p_a - q_a) if a < k  (residual distribution, Sec. 2.2)
+      p_k               if a = k  (the LLM's one additional token, Sec. 4.3)
+      p_a               if a < k and sum(w) == 0 (only reachable through rounding)
+  next = smallest v with sum_{t<=v} w_t > u_k * sum(w)   (inverse CDF, ids ascending)
+
+Tree (token-tree verification as in SpecInfer, cited in Sec. 5.1 and Sec. 6.1;
+the paper does not spell the rule out), read as: node n >= 1 is accepted iff
+its parent is accepted and u_{n-1} * q_par(x_n) < p_par(x_n), where par is
+its parent's target row and draft row; n* = the deepest accepted node,
+smallest BFS index on ties; accepted length = depth(n*); the final token is
+drawn from p_{n*} if n* is a leaf, else from max(0, p_{n*} - q_{n*}) (same
+zero-mass fallback).  For a path-shaped tree this is exactly the chain.
+
+Near ties.  A GPU computes p in fp32, so its decisions can legitimately
+differ from these fp64 ones only when a uniform lies within NEAR_TIE of a
+decision boundary: |u_j - min(1, p/q)| for an evaluated acceptance test, and
+the distance of the final uniform to the normalised CDF values bracketing the
+chosen token.  Every near tie on a request's decision path is reported.
+"""
+from __future__ import annotations
+
+from typing import Optional, Sequence
+
+import numpy as np
+
+from .attention import widen
+
+NEAR_TIE = 1e-5
+
+
+def softmax64(logits: np.ndarray) -> np.ndarray:
+    """Target distribution of one row (fp64, max-subtracted)."""
+    x = np.asarray(logits, dtype=np.float64)
+    e = np.exp(x - x.max())
+    return e / e.sum()
+
+
+def inverse_cdf(w: np.ndarray, u: float):
+    """Smallest v with cumsum(w)[v] > u * sum(w); also the normalised margin.
+
+    Zero-weight tokens are never chosen; a target that rounds past the total
+    is clamped to the last token with positive weight.
+    """
+    w = np.asarray(w, dtype=np.float64)
+    cdf = np.cumsum(w)
+    total = cdf[-1]
+    v = int(np.searchsorted(cdf, u * total, side="right"))
+    # cdf[v] > target >= cdf[v-1] forces w[v] > 0; only an overshoot needs a clamp
+    if v >= len(w):
+        v = int(np.nonzero(w > 0)[0][-1])
+    f_hi = cdf[v] / total
+    f_lo = cdf[v - 1] / total if v > 0 else 0.0
+    margin = min(abs(u - f_lo), abs(f_hi - u))
+    return v, margin
+
+
+def _test(u: float, px: float, qx: float):
+    """Acceptance test u*q(x) < p(x) and its distance to the boundary."""
+    accept = u * qx < px
+    if qx > 0:
+        margin = abs(u - min(1.0, px / qx))
+    else:
+        margin = np.inf
+    return bool(accept), margin
+
+
+def accept_chain(p_rows: np.ndarray, q_rows: np.ndarray, tokens: Sequence[int],
+                 uniforms: Sequence[float]) -> dict:
+    """One request of the chain rule.  p_rows [k+1, V] (target probabilities),
+    q_rows [k, V] (draft probabilities), tokens [k], uniforms [k+1]."""
+    k = len(tokens)
+    margins = []
+    a = k
+    for j in range(k):
+        x = int(tokens[j])
+        ok, m = _test(float(uniforms[j]), p_rows[j, x], q_rows[j, x])
+        margins.append(m)
+        if not ok:
+            a = j
+            break
+    if a < k:
+        w = np.maximum(0.0, p_rows[a] - q_rows[a])
+        if w.sum() <= 0.0:
+            w = p_rows[a]
+    else:
+        w = p_rows[k]
+    nxt, m_s = inverse_cdf(w, float(uniforms[k]))
+    margins.append(m_s)
+    return {"accepted_len": a, "next_token": nxt, "accepted_node": a,
+            "margin": float(min(margins)), "near_tie": bool(min(margins) < NEAR_TIE)}
+
+
+def tree_depths(parent: Sequence[int]) -> np.ndarray:
+    depth = np.zeros(len(parent), dtype=np.int64)
+    for n in range(1, len(parent)):
+        depth[n] = depth[int(parent[n])] + 1
+    return depth
+
+
+def accept_tree(p_rows: np.ndarray, q_rows: dict, tokens: Sequence[int],
+                uniforms: Sequence[float], parent: Sequence[int]) -> dict:
+    """One request of the tree rule.  p_rows [n, V]; q_rows maps each node that
+    has children to its draft row; tokens[n-1] is node n's token; uniforms [n]."""
+    n = len(parent)
+    depth = tree_depths(parent)
+    has_child = set(int(x) for x in parent[1:])
+    accepted = np.zeros(n, dtype=bool)
+    accepted[0] = True
+    margins = []
+    for node in range(1, n):
+        par = int(parent[node])
+        if not accepted[par]:
+            continue
+        x = int(tokens[node - 1])
+        ok, m = _test(float(uniforms[node - 1]), p_rows[par, x], q_rows[par][x])
+        margins.append(m)
+        accepted[node] = ok
+    best = 0
+    for node in range(1, n):
+        if accepted[node] and depth[node] > depth[best]:
+            best = node
+    if best in has_child:
+        w = np.maximum(0.0, p_rows[best] - q_rows[best])
+        if w.sum() <= 0.0:
+            w = p_rows[best]
+    else:
+        w = p_rows[best]
+    nxt, m_s = inverse_cdf(w, float(uniforms[n - 1]))
+    margins.append(m_s)
+    return {"accepted_len": int(depth[best]), "next_token": nxt, "accepted_node": best,
+            "margin": float(min(margins)), "near_tie": bool(min(margins) < NEAR_TIE)}
+
+
+def verify_accept(target_logits: np.ndarray, draft_probs: np.ndarray,
+                  draft_tokens: np.ndarray, uniforms: np.ndarray,
+                  n_q: Sequence[int], dtype: str = "f32",
+                  tree_parent: Optional[Sequence[int]] = None,
+                  requests: Optional[Sequence[int]] = None) -> dict:
+    """Acceptance for a packed batch (layouts as in the C interface).
+
+    Request i owns target rows q0_i .. q0_i + n_i - 1 (q0 = running sum of
+    n_i), uniforms at the same rows, draft tokens q0_i - i .. q0_i - i + n_i - 2
+    (one per non-root node) and draft rows d0_i .. (d0 = running sum of the
+    number of nodes with children: k_i for a chain).  ``requests`` restricts
+    the work to a subset (results for the others are -1).
+    """
+    n_q = [int(x) for x in n_q]
+    B = len(n_q)
+    if tree_parent is not None:
+        has_child = sorted(set(int(x) for x in tree_parent[1:]))
+        n_int = [len(has_child)] * B
+    else:
+        n_int = [n - 1 for n in n_q]
+    q0 = np.concatenate([[0], np.cumsum(n_q)]).astype(np.int64)
+    d0 = np.concatenate([[0], np.cumsum(n_int)]).astype(np.int64)
+    keys = ("accepted_len", "next_token", "accepted_node")
+    res = {key: np.full(B, -1, dtype=np.int64) for key in keys}
+    res["near_tie"] = np.zeros(B, dtype=bool)
+    res["margin"] = np.full(B, np.inf)
+    todo = range(B) if requests is None else requests
+    for i in todo:
+        n = n_q[i]
+        p_rows = np.stack([softmax64(widen(target_logits[q0[i] + j], dtype)) for j in range(n)])
+        toks = np.asarray(draft_tokens[q0[i] - i: q0[i] - i + n - 1], dtype=np.int64)
+        us = np.asarray(uniforms[q0[i]: q0[i] + n], dtype=np.float64)
+        if tree_parent is None:
+            q_rows = widen(draft_probs[d0[i]: d0[i] + n - 1], dtype).reshape(n - 1, -1)
+            r = accept_chain(p_rows, q_rows, toks, us)
+        else:
+            q_rows = {node: widen(draft_probs[d0[i] + rnk], dtype) for rnk, node in enumerate(has_child)}
+            r = accept_tree(p_rows, q_rows, toks, us, tree_parent)
+        for key in keys:
+            res[key][i] = r[key]
+        res["near_tie"][i] = r["near_tie"]
+        res["margin"][i] = r["margin"]
+    return res
