@@ -1,0 +1,165 @@
+"""Benchmark of the batched speculative-decoding verify step on one MI355X.
+
+A step is one spec_verify call over one batch: host plan + upload, split-KV
+verify attention (+ combine), acceptance and the final sample -- every row of
+the hot path -- over inputs already resident in HBM.  Prints ONE JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "verified tokens/s per verify step; achieved HBM GB/s vs MI355X peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mha7b_b32")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    return ap.parse_args()
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for name in ("attention.hip", "sv_internal.h"):
+        with open(os.path.join(ROOT, "paper_2505_17074_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the split-KV kernel from the committed rocprofv3
+    counter summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"attn_split_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    sha = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not sha or not val or sha.group(1) != kernel_source_digest():
+        return None
+    return float(val.group(1))
+
+
+def cpu_baseline(pool, budget_s: float):
+    """The fp64 oracle (untuned) on a bounded prefix of the same requests."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:                                   # pragma: no cover
+        threads = 1
+    q0, kv0, n_q = pool.q_start, pool.kv_start, pool.n_q
+    done_tokens, t_used, m = 0, 0.0, 0
+    while m < pool.batch and t_used < budget_s:
+        i = m
+        n, c = int(n_q[i]), int(pool.ctx_len[i])
+        t0 = time.perf_counter()
+        oracle.verify_attention(pool.q[q0[i]:q0[i] + n], pool.k[kv0[i]:kv0[i + 1]], pool.v[kv0[i]:kv0[i + 1]],
+                                [c], [n], pool.num_kv_heads, dtype=pool.qkv_dtype, tree_parent=pool.tree_parent)
+        oracle.verify_accept(pool.target_logits[q0[i]:q0[i] + n], pool.draft_probs[pool.d_start[i]:pool.d_start[i + 1]],
+                             pool.draft_tokens[q0[i] - i:q0[i] - i + n - 1], pool.uniforms[q0[i]:q0[i] + n], [n],
+                             dtype=pool.logit_dtype, tree_parent=pool.tree_parent)
+        t_used += time.perf_counter() - t0
+        done_tokens += n
+        m += 1
+    return {"value": done_tokens / t_used, "unit": "verified tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"first {m} of {pool.batch} requests ({done_tokens} verify tokens), "
+                      f"attention + acceptance in fp64 NumPy, {t_used:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); multi-GPU sharding of the verify step is "
+              "described in the design notes but not built", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2505_17074_amd import workload as W
+    from paper_2505_17074_amd.batch import DeviceBatch, Verifier
+
+    cfg = W.CONFIG_BY_NAME[args.workload]
+    pool = W.make_pool(cfg, args.seed)
+    work = W.workload_bytes(pool)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    batch = DeviceBatch(pool, dev)
+    ver = Verifier(batch)
+    stream = torch.cuda.current_stream(dev)
+
+    K, Wm = args.steps, args.warmup
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    for e4 in ev:
+        for e in e4:
+            e.record(stream)          # materialise the events
+    torch.cuda.synchronize()
+
+    for _ in range(Wm):
+        ver.run("verify", stream)
+    torch.cuda.synchronize()
+
+    t0 = time.perf_counter()
+    for k in range(K):
+        ver.attn.event_begin, ver.attn.event_end = ev[k][0].cuda_event, ev[k][1].cuda_event
+        ver.acc.event_begin, ver.acc.event_end = ev[k][2].cuda_event, ev[k][3].cuda_event
+        ver.run("verify", stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ver.attn.event_begin = ver.attn.event_end = ver.acc.event_begin = ver.acc.event_end = None
+
+    ms = (t1 - t0) * 1e3 / K
+    t_attn_us = float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]) * 1e3)
+    t_acc_us = float(np.mean([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)]) * 1e3)
+    achieved = work["attn_bytes"] / (t_attn_us * 1e-6) / 1e9
+    traffic = measured_traffic(args.workload)
+
+    line = {
+        "metric": METRIC,
+        "value": work["Nq"] / (ms * 1e-3),
+        "unit": "verified tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if pool.qkv_dtype == W.BF16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "requests": pool.batch, "verify_tokens": work["Nq"],
+                   "kv_tokens": work["Nkv"], "q_heads": pool.num_q_heads, "kv_heads": pool.num_kv_heads,
+                   "head_dim": pool.head_dim, "vocab": pool.vocab, "logits": pool.logit_dtype,
+                   "tree_nodes": 0 if pool.tree_parent is None else len(pool.tree_parent), "seed": args.seed},
+        "roofline": {"bound": "hbm", "kernel": "attn_split_mfma", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "algorithmic_bytes": work["attn_bytes"], "kernel_us": t_attn_us},
+        "accept": {"kernels_us": t_acc_us, "algorithmic_bytes_upper": work["accept_bytes"],
+                   "achieved_GBs": work["accept_bytes"] / (t_acc_us * 1e-6) / 1e9},
+    }
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(pool, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,222 @@
+/*
+ * specverify.h -- C ABI of the MI355X (gfx950) batched speculative-decoding
+ * verify step.
+ *
+ * One verify step serves the requests a speculative-decoding scheduler has
+ * picked for this round (the LAPS-SD setting of arXiv 2505.17074, Sec. 3:
+ * requests with a context, a draft of candidate tokens and a target model
+ * that verifies all of them in one parallel forward, Sec. 2.2).  For each
+ * request i with c_i cached KV positions and a draft of k_i tokens:
+ *
+ *   1. verify attention: the k_i + 1 verify queries (the last accepted token
+ *      plus the drafts) -- or the nodes of a token tree -- attend over the
+ *      request's cached keys and, inside the verify block, over their own
+ *      ancestors-or-self (causal for a chain, tree-ancestor for a tree);
+ *   2. acceptance: target softmax of each verify position, the acceptance
+ *      test of Eq. (1) (draft j is accepted iff u_j * q_j(x_j) < p_j(x_j),
+ *      i.e. u_j < min(1, p/q), with p the TARGET and q the DRAFT
+ *      distribution), the resample from the residual max(0, p - q) at the
+ *      first rejection (Sec. 2.2), or the target's one additional token when
+ *      every draft is accepted (Sec. 4.3, the "+1" of Eq. (6));
+ *   3. outputs: each request's accepted count a_i -- what the scheduler's
+ *      acceptance-rate estimate consumes (Sec. 4.3) -- and its next token.
+ *
+ * Conventions for every entry point
+ *   - Device pointers point to memory on the current HIP device; host
+ *     pointers are read during the call only.  The library keeps no pointer
+ *     after it returns and allocates no device memory: the caller passes a
+ *     device workspace and a pinned host staging buffer sized by
+ *     spec_workspace_bytes().
+ *   - `stream` is a hipStream_t (NULL = the null stream).  All device work
+ *     is enqueued on it in order; nothing synchronises the device.  Outputs
+ *     are valid once the stream has passed the call.
+ *   - The host staging buffer is written by the call and read by an
+ *     asynchronous copy on `stream`: it must stay untouched until the stream
+ *     has passed the call.  Calls in flight at the same time need separate
+ *     workspaces and staging buffers.
+ *   - All argument checks run on the host before any HIP call; on an error
+ *     nothing is enqueued and no output is touched.  Device-resident values
+ *     (token ids in [0, V), uniforms in [0, 1), finite logits) are the
+ *     caller's contract and are not checked.
+ *   - Results are deterministic: the same inputs give bit-identical outputs
+ *     (fixed reduction orders, no floating-point atomics).
+ */
+#ifndef SPECVERIFY_H
+#define SPECVERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define SPEC_API __attribute__((visibility("default")))
+#else
+#define SPEC_API
+#endif
+
+#define SPEC_ABI_VERSION 1
+#define SPEC_MAX_DRAFT 16        /* chain drafts per request */
+#define SPEC_MAX_TREE_NODES 32   /* token-tree nodes per request, root included */
+
+typedef enum spec_status {
+  SPEC_OK = 0,
+  SPEC_ERR_INVALID_ARG = 1,   /* a null pointer, size, stride or tree that breaks the contract */
+  SPEC_ERR_UNSUPPORTED = 2,   /* valid but not built: head_dim not 64/128, a dtype/shape combination */
+  SPEC_ERR_WORKSPACE = 3,     /* workspace or staging too small or misaligned */
+  SPEC_ERR_HIP = 4            /* a HIP runtime call failed (launch, copy) */
+} spec_status_t;
+
+typedef enum spec_dtype {
+  SPEC_F32 = 0,
+  SPEC_BF16 = 1
+} spec_dtype_t;
+
+/*
+ * The requests of one step (host memory).
+ *   num_requests  B >= 1.
+ *   ctx_len[B]    c_i >= 0: KV positions cached before the verify block.
+ *   draft_len[B]  chain mode: k_i in [0, SPEC_MAX_DRAFT] drafts (k_i = 0 is
+ *                 plain decoding: no test, one sample from the target).
+ *                 Ignored (may be NULL) in tree mode.
+ *   tree_nodes    0 = chain mode.  Otherwise every request verifies the same
+ *                 token-tree topology of tree_nodes nodes (1 ..
+ *                 SPEC_MAX_TREE_NODES), node 0 being the last accepted token.
+ *   tree_parent   [tree_nodes], BFS order: parent[0] = -1, 0 <= parent[n] < n.
+ *
+ * Derived counts: n_i = k_i + 1 (chain) or tree_nodes verify positions;
+ * Nq = sum n_i;  Nkv = sum (c_i + n_i);  Nd = sum of the number of nodes
+ * that have children (k_i for a chain).  Request i's rows of every packed
+ * array start at the running sum of the matching count over requests < i.
+ */
+typedef struct spec_requests {
+  int32_t num_requests;
+  const int32_t* ctx_len;
+  const int32_t* draft_len;
+  int32_t tree_nodes;
+  const int32_t* tree_parent;
+} spec_requests_t;
+
+/*
+ * Verify attention (device memory).
+ *   q     [Nq, Hq, d]  request i's verify positions (node order), strides
+ *         q_stride_tok / q_stride_head in elements, last dim contiguous.
+ *   k, v  [Nkv, Hkv, d] request i's c_i cached rows followed by its n_i
+ *         verify rows (already appended by the caller); shared strides
+ *         kv_stride_tok / kv_stride_head in elements, last dim contiguous.
+ *   out   [Nq, Hq, d] float32, contiguous.
+ *   Query head h reads KV head h / (Hq / Hkv).  scale <= 0 selects
+ *   1/sqrt(d).  dtype SPEC_BF16 (MFMA path) or SPEC_F32; d in {64, 128}.
+ *   split_kv 0 = automatic split of long contexts; otherwise the number of
+ *   KV positions per split (a positive multiple of 32) -- results agree
+ *   across splits within fp32 rounding.  Requests split more than once are
+ *   merged by a second (combine) kernel.
+ */
+typedef struct spec_attn_args {
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  spec_dtype_t dtype;
+  float scale;
+  const void* q;
+  int64_t q_stride_tok;
+  int64_t q_stride_head;
+  const void* k;
+  const void* v;
+  int64_t kv_stride_tok;
+  int64_t kv_stride_head;
+  float* out;
+  int32_t split_kv;
+  /* Optional profiling: hipEvent_t handles recorded on `stream` right before
+   * and right after the split-KV attention kernel (NULL = not recorded). */
+  void* event_begin;
+  void* event_end;
+} spec_attn_args_t;
+
+/*
+ * Acceptance and final sample (device memory).
+ *   target_logits [Nq, V]  row r = verify position r; row stride
+ *                 logits_stride elements (>= V).
+ *   draft_probs   [Nd, V]  the draft distribution of each node that has
+ *                 children, used as stored (not renormalised); row stride
+ *                 probs_stride.  Same dtype as target_logits.
+ *   draft_tokens  [Nq - B] int32, one per non-root node: request i's are at
+ *                 q0_i - i .. q0_i - i + n_i - 2 (node n at offset n - 1).
+ *   uniforms      [Nq] float32 in [0, 1): request i's node n >= 1 is tested
+ *                 with uniforms[q0_i + n - 1]; uniforms[q0_i + n_i - 1]
+ *                 drives the final sample.
+ *   accepted_len  [B] out: accepted drafts a_i (tree: depth of the deepest
+ *                 accepted node).
+ *   next_token    [B] out: the token sampled after the accepted prefix.
+ *   accepted_node [B] out (may be NULL): the deepest accepted node (chain:
+ *                 equals accepted_len).
+ * Tree reading: node n is accepted iff its parent is and its own test
+ * passes against the parent's target and draft rows; the deepest accepted
+ * node wins, the smallest BFS index on ties; the final token is drawn from
+ * that node's target row if it is a leaf, else from the residual.
+ * Inverse-CDF convention: token ids ascending, the smallest id whose
+ * cumulative weight exceeds u * (total weight); zero weights never chosen.
+ */
+typedef struct spec_accept_args {
+  int32_t vocab;
+  spec_dtype_t dtype;
+  const void* target_logits;
+  int64_t logits_stride;
+  const void* draft_probs;
+  int64_t probs_stride;
+  const int32_t* draft_tokens;
+  const float* uniforms;
+  int32_t* accepted_len;
+  int32_t* next_token;
+  int32_t* accepted_node;
+  /* Optional profiling: hipEvent_t handles recorded on `stream` right before
+   * the first and right after the last acceptance kernel (NULL = none). */
+  void* event_begin;
+  void* event_end;
+} spec_accept_args_t;
+
+/* Workspace sizes for a call with these arguments (either args pointer may
+ * be NULL when that part is not run).  The device workspace must be
+ * 256-byte aligned; the host staging buffer should be pinned
+ * (hipHostMalloc) for the copy to be asynchronous. */
+SPEC_API spec_status_t spec_workspace_bytes(const spec_requests_t* req,
+                                   const spec_attn_args_t* attn,
+                                   const spec_accept_args_t* acc,
+                                   size_t* device_bytes,
+                                   size_t* host_bytes);
+
+/* Step 1 alone: verify attention into attn->out. */
+SPEC_API spec_status_t spec_verify_attn(const spec_requests_t* req,
+                               const spec_attn_args_t* attn,
+                               void* workspace, size_t workspace_bytes,
+                               void* host_staging, size_t host_staging_bytes,
+                               void* stream);
+
+/* Steps 2-3 alone: acceptance and the final sample. */
+SPEC_API spec_status_t spec_accept(const spec_requests_t* req,
+                          const spec_accept_args_t* acc,
+                          void* workspace, size_t workspace_bytes,
+                          void* host_staging, size_t host_staging_bytes,
+                          void* stream);
+
+/* The whole verify step: attention then acceptance on one stream with one
+ * plan upload (the logits are inputs, so the two parts are independent). */
+SPEC_API spec_status_t spec_verify(const spec_requests_t* req,
+                          const spec_attn_args_t* attn,
+                          const spec_accept_args_t* acc,
+                          void* workspace, size_t workspace_bytes,
+                          void* host_staging, size_t host_staging_bytes,
+                          void* stream);
+
+/* Static text for a status code. */
+SPEC_API const char* spec_status_str(spec_status_t status);
+
+/* SPEC_ABI_VERSION of the built library. */
+SPEC_API int32_t spec_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPECVERIFY_H */

@@ -178,7 +178,7 @@ def verify_accept(target_logits: np.ndarray, draft_probs: np.ndarray,
         toks = np.asarray(draft_tokens[q0[i] - i: q0[i] - i + n - 1], dtype=np.int64)
         us = np.asarray(uniforms[q0[i]: q0[i] + n], dtype=np.float64)
         if tree_parent is None:
-            q_rows = widen(draft_probs[d0[i]: d0[i] + n - 1], dtype).reshape(n - 1, -1)
+            q_rows = widen(draft_probs[d0[i]: d0[i] + n - 1], dtype).reshape(n - 1, target_logits.shape[1])
             r = accept_chain(p_rows, q_rows, toks, us)
         else:
             q_rows = {node: widen(draft_probs[d0[i] + rnk], dtype) for rnk, node in enumerate(has_child)}

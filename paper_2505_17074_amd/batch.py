@@ -1,0 +1,140 @@
+"""Packed device batches and a verifier that drives the C ABI.
+
+PyTorch is used for device memory, pinned host memory, streams and events
+only; every step of the verify path runs in the library's HIP kernels.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from typing import Optional
+
+import numpy as np
+import torch
+
+from . import binding as B
+from .workload import BF16, F32, Pool
+
+
+def _to_device(arr: np.ndarray, dtype: str, device) -> torch.Tensor:
+    if dtype == BF16:
+        return torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).view(torch.bfloat16).to(device)
+    if dtype == F32:
+        return torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32)).to(device)
+    raise ValueError(dtype)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+class DeviceBatch:
+    """One verify step's packed inputs and outputs resident in device memory."""
+
+    def __init__(self, pool: Pool, device="cuda"):
+        self.pool = pool
+        self.device = torch.device(device)
+        self.q = _to_device(pool.q, pool.qkv_dtype, self.device)
+        self.k = _to_device(pool.k, pool.qkv_dtype, self.device)
+        self.v = _to_device(pool.v, pool.qkv_dtype, self.device)
+        self.logits = _to_device(pool.target_logits, pool.logit_dtype, self.device)
+        self.probs = _to_device(pool.draft_probs, pool.logit_dtype, self.device)
+        self.tokens = torch.from_numpy(pool.draft_tokens.astype(np.int32)).to(self.device)
+        self.uniforms = torch.from_numpy(pool.uniforms.astype(np.float32)).to(self.device)
+        Nq, Hq, d = pool.q.shape
+        self.out = torch.empty((Nq, Hq, d), dtype=torch.float32, device=self.device)
+        Bn = pool.batch
+        self.accepted_len = torch.empty(Bn, dtype=torch.int32, device=self.device)
+        self.next_token = torch.empty(Bn, dtype=torch.int32, device=self.device)
+        self.accepted_node = torch.empty(Bn, dtype=torch.int32, device=self.device)
+
+    def requests(self) -> B.SpecRequests:
+        p = self.pool
+        if p.tree_parent is not None:
+            return B.make_requests(p.ctx_len, None, p.tree_parent)
+        return B.make_requests(p.ctx_len, p.draft_len)
+
+    def attn_args(self, split_kv: int = 0, scale: float = 0.0) -> B.SpecAttnArgs:
+        p = self.pool
+        a = B.SpecAttnArgs()
+        a.num_q_heads, a.num_kv_heads, a.head_dim = p.num_q_heads, p.num_kv_heads, p.head_dim
+        a.dtype = B.SPEC_BF16 if p.qkv_dtype == BF16 else B.SPEC_F32
+        a.scale = scale
+        a.q, a.k, a.v, a.out = _ptr(self.q), _ptr(self.k), _ptr(self.v), _ptr(self.out)
+        a.q_stride_tok, a.q_stride_head = self.q.stride(0), self.q.stride(1)
+        a.kv_stride_tok, a.kv_stride_head = self.k.stride(0), self.k.stride(1)
+        a.split_kv = split_kv
+        return a
+
+    def accept_args(self, with_node: bool = True) -> B.SpecAcceptArgs:
+        p = self.pool
+        a = B.SpecAcceptArgs()
+        a.vocab = p.vocab
+        a.dtype = B.SPEC_BF16 if p.logit_dtype == BF16 else B.SPEC_F32
+        a.target_logits, a.logits_stride = _ptr(self.logits), self.logits.stride(0)
+        a.draft_probs = _ptr(self.probs) if self.probs.numel() else None
+        a.probs_stride = self.probs.stride(0) if self.probs.numel() else p.vocab
+        a.draft_tokens = _ptr(self.tokens) if self.tokens.numel() else None
+        a.uniforms = _ptr(self.uniforms)
+        a.accepted_len, a.next_token = _ptr(self.accepted_len), _ptr(self.next_token)
+        a.accepted_node = _ptr(self.accepted_node) if with_node else None
+        return a
+
+
+class Verifier:
+    """Runs spec_verify / spec_verify_attn / spec_accept on one DeviceBatch.
+
+    Owns the device workspace and a ring of pinned staging buffers; before a
+    staging slot is rewritten, the event recorded after its previous call is
+    waited on, so calls may be issued back to back without a device sync.
+    """
+
+    def __init__(self, batch: DeviceBatch, split_kv: int = 0, ring: int = 3):
+        self.batch = batch
+        self.req = batch.requests()
+        self.attn = batch.attn_args(split_kv)
+        self.acc = batch.accept_args()
+        st, dev, host = B.spec_workspace_bytes(self.req, self.attn, self.acc)
+        B.check(st, "spec_workspace_bytes")
+        self.ws_bytes = dev
+        self._ws = torch.empty(dev + 256, dtype=torch.uint8, device=batch.device)
+        self.ws_ptr = (self._ws.data_ptr() + 255) // 256 * 256
+        self.staging_bytes = host
+        self._staging = [torch.empty(max(host, 1), dtype=torch.uint8, pin_memory=True) for _ in range(ring)]
+        self._events = [None] * ring
+        self._i = 0
+
+    def _slot(self):
+        s = self._i % len(self._staging)
+        self._i += 1
+        if self._events[s] is not None:
+            self._events[s].synchronize()
+        return s
+
+    def _done(self, s, stream):
+        ev = torch.cuda.Event()
+        ev.record(stream)
+        self._events[s] = ev
+
+    def run(self, which: str = "verify", stream: Optional[torch.cuda.Stream] = None) -> None:
+        stream = stream or torch.cuda.current_stream(self.batch.device)
+        s = self._slot()
+        stg = self._staging[s].data_ptr()
+        h = stream.cuda_stream
+        if which == "verify":
+            st = B.spec_verify(self.req, self.attn, self.acc, self.ws_ptr, self.ws_bytes, stg, self.staging_bytes, h)
+        elif which == "attn":
+            st = B.spec_verify_attn(self.req, self.attn, self.ws_ptr, self.ws_bytes, stg, self.staging_bytes, h)
+        elif which == "accept":
+            st = B.spec_accept(self.req, self.acc, self.ws_ptr, self.ws_bytes, stg, self.staging_bytes, h)
+        else:
+            raise ValueError(which)
+        B.check(st, f"spec_{which}")
+        self._done(s, stream)
+
+    def results(self) -> dict:
+        torch.cuda.synchronize(self.batch.device)
+        b = self.batch
+        return {"out": b.out.cpu().numpy(),
+                "accepted_len": b.accepted_len.cpu().numpy(),
+                "next_token": b.next_token.cpu().numpy(),
+                "accepted_node": b.accepted_node.cpu().numpy()}

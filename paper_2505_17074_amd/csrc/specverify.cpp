@@ -1,0 +1,390 @@
+// C ABI of the verify step: argument checks, the host plan, workspace
+// layout and the launch sequence.  Every check runs before the first HIP call.
+#include "../../include/specverify.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "sv_internal.h"
+
+namespace {
+
+using sv::AttnItem;
+using sv::ReqInfo;
+using sv::Topo;
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Plan {
+  // request view
+  int B = 0;
+  bool tree = false;
+  int64_t Nq = 0, Nkv = 0, Nd = 0;
+  std::vector<ReqInfo> reqs;
+  std::vector<int32_t> row_req;
+  Topo topo{};
+  // attention
+  bool has_attn = false;
+  std::vector<AttnItem> items;
+  int64_t parts = 0;      // partial rows
+  int nr_max = 1;
+  int split = 0;
+  // acceptance
+  bool has_acc = false;
+  int nch = 0;
+  // layout (bytes)
+  size_t off_topo = 0, off_reqs = 0, off_items = 0, off_rowreq = 0, plan_bytes = 0;
+  size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_decision = 0, off_masses = 0;
+  size_t device_bytes = 0;
+};
+
+spec_status_t check_requests(const spec_requests_t* r) {
+  if (!r || r->num_requests < 1 || !r->ctx_len) return SPEC_ERR_INVALID_ARG;
+  if (r->tree_nodes < 0 || r->tree_nodes > SPEC_MAX_TREE_NODES) return SPEC_ERR_INVALID_ARG;
+  if (r->tree_nodes > 0) {
+    if (!r->tree_parent || r->tree_parent[0] != -1) return SPEC_ERR_INVALID_ARG;
+    for (int n = 1; n < r->tree_nodes; ++n)
+      if (r->tree_parent[n] < 0 || r->tree_parent[n] >= n) return SPEC_ERR_INVALID_ARG;
+  } else if (!r->draft_len) {
+    return SPEC_ERR_INVALID_ARG;
+  }
+  int64_t nq = 0, nkv = 0;
+  for (int i = 0; i < r->num_requests; ++i) {
+    if (r->ctx_len[i] < 0) return SPEC_ERR_INVALID_ARG;
+    int n = r->tree_nodes;
+    if (n == 0) {
+      if (r->draft_len[i] < 0 || r->draft_len[i] > SPEC_MAX_DRAFT) return SPEC_ERR_INVALID_ARG;
+      n = r->draft_len[i] + 1;
+    }
+    nq += n;
+    nkv += (int64_t)r->ctx_len[i] + n;
+  }
+  if (nq >= INT32_MAX / 2 || nkv >= INT32_MAX / 2) return SPEC_ERR_INVALID_ARG;
+  return SPEC_OK;
+}
+
+spec_status_t check_attn(const spec_attn_args_t* a) {
+  if (!a) return SPEC_ERR_INVALID_ARG;
+  if (a->num_q_heads < 1 || a->num_kv_heads < 1 || a->num_q_heads % a->num_kv_heads)
+    return SPEC_ERR_INVALID_ARG;
+  if (a->dtype != SPEC_F32 && a->dtype != SPEC_BF16) return SPEC_ERR_INVALID_ARG;
+  if (a->head_dim != 64 && a->head_dim != 128) return SPEC_ERR_UNSUPPORTED;
+  if (!a->q || !a->k || !a->v || !a->out) return SPEC_ERR_INVALID_ARG;
+  if (!aligned16(a->q) || !aligned16(a->k) || !aligned16(a->v) || !aligned16(a->out))
+    return SPEC_ERR_INVALID_ARG;
+  const int64_t vec = a->dtype == SPEC_F32 ? 4 : 8;   // elements per 16 bytes
+  if (a->q_stride_tok < 1 || a->q_stride_head < 1 || a->kv_stride_tok < 1 || a->kv_stride_head < 1)
+    return SPEC_ERR_INVALID_ARG;
+  if (a->q_stride_tok % vec || a->q_stride_head % vec || a->kv_stride_tok % vec || a->kv_stride_head % vec)
+    return SPEC_ERR_INVALID_ARG;
+  if (a->split_kv < 0 || (a->split_kv > 0 && a->split_kv % 32)) return SPEC_ERR_INVALID_ARG;
+  return SPEC_OK;
+}
+
+spec_status_t check_accept(const spec_accept_args_t* a, int64_t Nq, int B) {
+  if (!a) return SPEC_ERR_INVALID_ARG;
+  if (a->dtype != SPEC_F32 && a->dtype != SPEC_BF16) return SPEC_ERR_INVALID_ARG;
+  if (a->vocab < 1 || (int64_t)a->vocab > (int64_t)sv::kAccMaxChunks * sv::kAccChunk) return SPEC_ERR_INVALID_ARG;
+  if (!a->target_logits || !a->uniforms || !a->accepted_len || !a->next_token) return SPEC_ERR_INVALID_ARG;
+  if (Nq > B && (!a->draft_probs || !a->draft_tokens)) return SPEC_ERR_INVALID_ARG;
+  const int64_t vec = a->dtype == SPEC_F32 ? 4 : 8;
+  if (a->logits_stride < a->vocab || a->logits_stride % vec || !aligned16(a->target_logits))
+    return SPEC_ERR_INVALID_ARG;
+  if (a->draft_probs && (a->probs_stride < a->vocab || a->probs_stride % vec || !aligned16(a->draft_probs)))
+    return SPEC_ERR_INVALID_ARG;
+  return SPEC_OK;
+}
+
+// Keys per split: enough work items to fill the chip, long enough that the
+// partial outputs stay small next to the KV bytes they summarise.
+int auto_split(int64_t key_streams, int rows_max) {
+  const int64_t target_items = 2048;
+  int64_t s = (key_streams + target_items - 1) / target_items;
+  s = std::max<int64_t>(s, std::max(256, 8 * rows_max));
+  s = (s + 31) / 32 * 32;
+  return (int)std::min<int64_t>(s, 1 << 20);
+}
+
+spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
+                         const spec_accept_args_t* acc, Plan& P) {
+  spec_status_t st = check_requests(r);
+  if (st != SPEC_OK) return st;
+  P.B = r->num_requests;
+  P.tree = r->tree_nodes > 0;
+  if (attn) {
+    st = check_attn(attn);
+    if (st != SPEC_OK) return st;
+  }
+
+  // topology tables
+  std::memset(&P.topo, 0, sizeof(P.topo));
+  const int tn = r->tree_nodes;
+  int n_int = 0;
+  for (int n = 0; n < sv::kMaxNodes; ++n) {
+    P.topo.parent[n] = n - 1;
+    P.topo.qrank[n] = -1;
+    P.topo.depth[n] = n;
+    P.topo.anc[n] = (n >= 31) ? 0xffffffffu : ((2u << n) - 1u);   // chain: nodes 0..n
+  }
+  if (P.tree) {
+    std::vector<bool> has_child(tn, false);
+    for (int n = 1; n < tn; ++n) has_child[r->tree_parent[n]] = true;
+    for (int n = 0; n < tn; ++n) {
+      P.topo.parent[n] = r->tree_parent[n];
+      P.topo.depth[n] = n == 0 ? 0 : P.topo.depth[r->tree_parent[n]] + 1;
+      P.topo.anc[n] = (1u << n) | (n == 0 ? 0u : P.topo.anc[r->tree_parent[n]]);
+      P.topo.qrank[n] = has_child[n] ? n_int++ : -1;
+    }
+    P.topo.nodes = tn;
+  }
+
+  // requests
+  P.reqs.resize(P.B);
+  int64_t q0 = 0, kv0 = 0, d0 = 0;
+  for (int i = 0; i < P.B; ++i) {
+    ReqInfo& q = P.reqs[i];
+    q.ctx = r->ctx_len[i];
+    q.nq = P.tree ? tn : r->draft_len[i] + 1;
+    q.q0 = (int32_t)q0;
+    q.kv0 = (int32_t)kv0;
+    q.d0 = (int32_t)d0;
+    q.nseg = 1;
+    q.part0 = 0;
+    q0 += q.nq;
+    kv0 += (int64_t)q.ctx + q.nq;
+    d0 += P.tree ? n_int : q.nq - 1;
+  }
+  P.Nq = q0;
+  P.Nkv = kv0;
+  P.Nd = d0;
+  P.row_req.resize(P.Nq);
+  for (int i = 0; i < P.B; ++i)
+    for (int j = 0; j < P.reqs[i].nq; ++j) P.row_req[P.reqs[i].q0 + j] = i;
+
+  if (acc) {
+    st = check_accept(acc, P.Nq, P.B);
+    if (st != SPEC_OK) return st;
+    P.has_acc = true;
+    P.nch = (acc->vocab + sv::kAccChunk - 1) / sv::kAccChunk;
+  }
+
+  if (attn) {
+    P.has_attn = true;
+    const int bf = attn->dtype == SPEC_BF16;
+    const int D = attn->head_dim;
+    const int Hq = attn->num_q_heads, Hkv = attn->num_kv_heads, G = Hq / Hkv;
+    const int rmax = sv::max_rows_per_item(bf, D);
+    // query-head groups per request so that heads * n_i <= rmax
+    std::vector<int> groups(P.B), hpg(P.B);
+    int64_t streams = 0;
+    int rows_max = 1;
+    for (int i = 0; i < P.B; ++i) {
+      const int n = P.reqs[i].nq;
+      const int ng = (G * n + rmax - 1) / rmax;
+      hpg[i] = (G + ng - 1) / ng;
+      groups[i] = (G + hpg[i] - 1) / hpg[i];
+      streams += ((int64_t)P.reqs[i].ctx + n) * Hkv * groups[i];
+      rows_max = std::max(rows_max, hpg[i] * n);
+    }
+    P.split = attn->split_kv > 0 ? attn->split_kv : auto_split(streams, rows_max);
+    int64_t part = 0;
+    int nr = 1;
+    for (int i = 0; i < P.B; ++i) {
+      ReqInfo& q = P.reqs[i];
+      const int L = q.ctx + q.nq;
+      q.nseg = (L + P.split - 1) / P.split;
+      q.part0 = (int32_t)part;
+      if (q.nseg > 1) part += (int64_t)q.nseg * q.nq * Hq;
+      for (int s = 0; s < q.nseg; ++s) {
+        for (int g = 0; g < Hkv; ++g) {
+          for (int gr = 0; gr < groups[i]; ++gr) {
+            AttnItem it;
+            it.req = i;
+            it.kvh = g;
+            it.head_lo = g * G + gr * hpg[i];
+            it.nheads = std::min(hpg[i], G - gr * hpg[i]);
+            it.kb = s * P.split;
+            it.ke = std::min(L, (s + 1) * P.split);
+            it.seg = q.nseg > 1 ? s : -1;
+            it.pad = 0;
+            P.items.push_back(it);
+            nr = std::max(nr, (it.nheads * q.nq + 15) / 16);
+          }
+        }
+      }
+    }
+    if (part >= INT32_MAX) return SPEC_ERR_INVALID_ARG;
+    P.parts = part;
+    P.nr_max = nr;
+  }
+
+  // layout: the plan block (uploaded), then device-only scratch
+  size_t off = 0;
+  P.off_topo = off;
+  off = align_up(off + sizeof(Topo));
+  P.off_reqs = off;
+  off = align_up(off + sizeof(ReqInfo) * P.B);
+  P.off_items = off;
+  off = align_up(off + sizeof(AttnItem) * P.items.size());
+  P.off_rowreq = off;
+  off = align_up(off + sizeof(int32_t) * P.Nq);
+  P.plan_bytes = off;
+  const int D = attn ? attn->head_dim : 0;
+  P.off_part_o = off;
+  off = align_up(off + sizeof(float) * (size_t)P.parts * D);
+  P.off_part_ml = off;
+  off = align_up(off + sizeof(float) * 2 * (size_t)P.parts);
+  P.off_rowstats = off;
+  off = align_up(off + sizeof(float) * 2 * (size_t)(P.has_acc ? P.Nq * P.nch : 0));
+  P.off_decision = off;
+  off = align_up(off + sizeof(int32_t) * 8 * (size_t)(P.has_acc ? P.B : 0));
+  P.off_masses = off;
+  off = align_up(off + sizeof(float) * (size_t)(P.has_acc ? (int64_t)P.B * P.nch : 0));
+  P.device_bytes = off;
+  return SPEC_OK;
+}
+
+void write_staging(const Plan& P, void* host) {
+  char* h = static_cast<char*>(host);
+  std::memset(h, 0, P.plan_bytes);
+  std::memcpy(h + P.off_topo, &P.topo, sizeof(Topo));
+  std::memcpy(h + P.off_reqs, P.reqs.data(), sizeof(ReqInfo) * P.reqs.size());
+  if (!P.items.empty()) std::memcpy(h + P.off_items, P.items.data(), sizeof(AttnItem) * P.items.size());
+  std::memcpy(h + P.off_rowreq, P.row_req.data(), sizeof(int32_t) * P.row_req.size());
+}
+
+spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, const spec_accept_args_t* acc,
+                  void* ws, size_t ws_bytes, void* staging, size_t staging_bytes, void* stream) {
+  Plan P;
+  spec_status_t st = build_plan(req, attn, acc, P);
+  if (st != SPEC_OK) return st;
+  if (!ws || (reinterpret_cast<uintptr_t>(ws) % kAlign) || ws_bytes < P.device_bytes) return SPEC_ERR_WORKSPACE;
+  if (!staging || staging_bytes < P.plan_bytes) return SPEC_ERR_WORKSPACE;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* d = static_cast<char*>(ws);
+  write_staging(P, staging);
+  if (hipMemcpyAsync(d, staging, P.plan_bytes, hipMemcpyHostToDevice, s) != hipSuccess) return SPEC_ERR_HIP;
+
+  const ReqInfo* reqs = reinterpret_cast<const ReqInfo*>(d + P.off_reqs);
+  const Topo* topo = reinterpret_cast<const Topo*>(d + P.off_topo);
+  const int32_t* row_req = reinterpret_cast<const int32_t*>(d + P.off_rowreq);
+
+  if (attn) {
+    sv::AttnParams a{};
+    a.q = attn->q;
+    a.k = attn->k;
+    a.v = attn->v;
+    a.q_st = attn->q_stride_tok;
+    a.q_sh = attn->q_stride_head;
+    a.kv_st = attn->kv_stride_tok;
+    a.kv_sh = attn->kv_stride_head;
+    a.out = attn->out;
+    a.part_o = reinterpret_cast<float*>(d + P.off_part_o);
+    a.part_ml = reinterpret_cast<float2*>(d + P.off_part_ml);
+    a.items = reinterpret_cast<const AttnItem*>(d + P.off_items);
+    a.reqs = reqs;
+    a.topo = topo;
+    a.row_req = row_req;
+    const float scale = attn->scale > 0.f ? attn->scale : 1.f / std::sqrt((float)attn->head_dim);
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.Hq = attn->num_q_heads;
+    a.Hkv = attn->num_kv_heads;
+    a.G = a.Hq / a.Hkv;
+    a.D = attn->head_dim;
+    a.n_items = (int32_t)P.items.size();
+    a.Nq = (int32_t)P.Nq;
+    if (attn->event_begin && hipEventRecord(static_cast<hipEvent_t>(attn->event_begin), s) != hipSuccess)
+      return SPEC_ERR_HIP;
+    if (sv::launch_attention(a, attn->dtype == SPEC_BF16, P.nr_max, s) != hipSuccess) return SPEC_ERR_HIP;
+    if (attn->event_end && hipEventRecord(static_cast<hipEvent_t>(attn->event_end), s) != hipSuccess)
+      return SPEC_ERR_HIP;
+    if (P.parts > 0 && sv::launch_combine(a, s) != hipSuccess) return SPEC_ERR_HIP;
+  }
+  if (acc) {
+    sv::AccParams c{};
+    c.logits = acc->target_logits;
+    c.probs = acc->draft_probs ? acc->draft_probs : acc->target_logits;
+    c.l_st = acc->logits_stride;
+    c.p_st = acc->draft_probs ? acc->probs_stride : acc->logits_stride;
+    c.tokens = acc->draft_tokens;
+    c.uniforms = acc->uniforms;
+    c.acc_len = acc->accepted_len;
+    c.next_tok = acc->next_token;
+    c.acc_node = acc->accepted_node;
+    c.reqs = reqs;
+    c.topo = topo;
+    c.row_req = row_req;
+    c.rowstats = reinterpret_cast<float2*>(d + P.off_rowstats);
+    c.decision = reinterpret_cast<int32_t*>(d + P.off_decision);
+    c.masses = reinterpret_cast<float*>(d + P.off_masses);
+    c.V = acc->vocab;
+    c.nch = P.nch;
+    c.B = P.B;
+    c.Nq = (int32_t)P.Nq;
+    c.tree = P.tree ? 1 : 0;
+    c.bf16 = acc->dtype == SPEC_BF16;
+    if (acc->event_begin && hipEventRecord(static_cast<hipEvent_t>(acc->event_begin), s) != hipSuccess)
+      return SPEC_ERR_HIP;
+    if (sv::launch_accept(c, s) != hipSuccess) return SPEC_ERR_HIP;
+    if (acc->event_end && hipEventRecord(static_cast<hipEvent_t>(acc->event_end), s) != hipSuccess)
+      return SPEC_ERR_HIP;
+  }
+  return SPEC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+spec_status_t spec_workspace_bytes(const spec_requests_t* req, const spec_attn_args_t* attn,
+                                   const spec_accept_args_t* acc, size_t* device_bytes, size_t* host_bytes) {
+  if (!device_bytes || !host_bytes) return SPEC_ERR_INVALID_ARG;
+  Plan P;
+  const spec_status_t st = build_plan(req, attn, acc, P);
+  if (st != SPEC_OK) return st;
+  *device_bytes = P.device_bytes;
+  *host_bytes = P.plan_bytes;
+  return SPEC_OK;
+}
+
+spec_status_t spec_verify_attn(const spec_requests_t* req, const spec_attn_args_t* attn, void* workspace,
+                               size_t workspace_bytes, void* host_staging, size_t host_staging_bytes,
+                               void* stream) {
+  if (!attn) return SPEC_ERR_INVALID_ARG;
+  return run(req, attn, nullptr, workspace, workspace_bytes, host_staging, host_staging_bytes, stream);
+}
+
+spec_status_t spec_accept(const spec_requests_t* req, const spec_accept_args_t* acc, void* workspace,
+                          size_t workspace_bytes, void* host_staging, size_t host_staging_bytes, void* stream) {
+  if (!acc) return SPEC_ERR_INVALID_ARG;
+  return run(req, nullptr, acc, workspace, workspace_bytes, host_staging, host_staging_bytes, stream);
+}
+
+spec_status_t spec_verify(const spec_requests_t* req, const spec_attn_args_t* attn, const spec_accept_args_t* acc,
+                          void* workspace, size_t workspace_bytes, void* host_staging, size_t host_staging_bytes,
+                          void* stream) {
+  if (!attn || !acc) return SPEC_ERR_INVALID_ARG;
+  return run(req, attn, acc, workspace, workspace_bytes, host_staging, host_staging_bytes, stream);
+}
+
+const char* spec_status_str(spec_status_t status) {
+  switch (status) {
+    case SPEC_OK: return "ok";
+    case SPEC_ERR_INVALID_ARG: return "invalid argument";
+    case SPEC_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case SPEC_ERR_WORKSPACE: return "workspace or staging buffer too small or misaligned";
+    case SPEC_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+int32_t spec_abi_version(void) { return SPEC_ABI_VERSION; }
+
+}  // extern "C"

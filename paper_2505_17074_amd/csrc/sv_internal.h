@@ -1,0 +1,93 @@
+// Internal layout shared by the host planner and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sv {
+
+constexpr int kMaxNodes = 32;          // verify positions per request (chain k+1 or tree)
+constexpr int kAccChunk = 4096;        // vocabulary entries per acceptance work-group
+constexpr int kAccThreads = 256;
+
+// One request of the step, as the kernels see it.
+struct ReqInfo {
+  int32_t ctx;      // c_i
+  int32_t nq;       // n_i verify positions
+  int32_t q0;       // first query / target-logit / uniform row
+  int32_t kv0;      // first KV row
+  int32_t d0;       // first draft-probability row
+  int32_t nseg;     // KV splits of this request (1 = direct output)
+  int32_t part0;    // first partial row (nseg > 1)
+  int32_t pad;
+};
+
+// One attention work item: a KV range of one (request, KV head, query-head group).
+struct AttnItem {
+  int32_t req;
+  int32_t kvh;
+  int32_t head_lo;  // first query head of the group
+  int32_t nheads;   // query heads in the group (rows = nheads * n_i)
+  int32_t kb, ke;   // KV positions [kb, ke) relative to the request's first KV row
+  int32_t seg;      // split index (partial slot) or -1 for direct output
+  int32_t pad;
+};
+
+// Tree / chain topology tables (one per step).
+struct Topo {
+  uint32_t anc[kMaxNodes];    // ancestors-or-self bit mask of each node
+  int32_t parent[kMaxNodes];  // -1 for the root
+  int32_t qrank[kMaxNodes];   // draft-probability row of a node with children, else -1
+  int32_t depth[kMaxNodes];
+  int32_t nodes;              // tree nodes (tree mode) or 0 (chain)
+  int32_t pad[3];
+};
+
+struct AttnParams {
+  const void* q;
+  const void* k;
+  const void* v;
+  int64_t q_st, q_sh, kv_st, kv_sh;   // element strides
+  float* out;
+  float* part_o;      // [P, d] unnormalised partial outputs
+  float2* part_ml;    // [P] (running max in log2 units, running sum)
+  const AttnItem* items;
+  const ReqInfo* reqs;
+  const Topo* topo;
+  const int32_t* row_req;   // query row -> request
+  float scale_log2;   // scale * log2(e)
+  int32_t Hq, Hkv, G, D;
+  int32_t n_items;
+  int32_t Nq;
+};
+
+struct AccParams {
+  const void* logits;
+  const void* probs;
+  int64_t l_st, p_st;
+  const int32_t* tokens;
+  const float* uniforms;
+  int32_t* acc_len;
+  int32_t* next_tok;
+  int32_t* acc_node;
+  const ReqInfo* reqs;
+  const Topo* topo;
+  const int32_t* row_req;
+  float2* rowstats;    // [Nq, nch] (chunk max, chunk sum of exp)
+  int32_t* decision;   // [B, 8]: accepted node, sample row, draft row or -1, accepted len, M, Z bits
+  float* masses;       // [B, nch]
+  int32_t V, nch, B, Nq;
+  int32_t tree;        // 1 = tree mode
+  int32_t bf16;
+};
+
+constexpr int kAccMaxChunks = 1024;    // vocabularies up to 4M entries
+
+// Largest number of query rows (heads x verify positions) one work item holds.
+int max_rows_per_item(int dtype_bf16, int D);
+
+hipError_t launch_attention(const AttnParams& p, int dtype_bf16, int nr_max, hipStream_t s);
+hipError_t launch_combine(const AttnParams& p, hipStream_t s);
+hipError_t launch_accept(const AccParams& p, hipStream_t s);
+
+}  // namespace sv

@@ -1,0 +1,190 @@
+"""The C ABI on a GPU-less host: exported symbols, status strings, and every
+argument check (which must run before the first HIP call)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2505_17074_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "specverify.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2505_17074_amd import build
+        build.build()
+    return B.load()
+
+
+def _declared():
+    text = open(HEADER).read()
+    return re.findall(r"SPEC_API\s+[\w\s\*]+?\b(spec_\w+)\s*\(", text)
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert set(names) == set(B.EXPORTS)
+    for name in names:
+        assert hasattr(lib, name), name
+    nm = os.popen(f"nm -D --defined-only {B.LIB_PATH}").read()
+    exported = set(re.findall(r"\bT (spec_\w+)", nm))
+    assert exported == set(names)
+
+
+def test_version_and_status_strings(lib):
+    text = open(HEADER).read()
+    assert B.spec_abi_version() == int(re.search(r"#define SPEC_ABI_VERSION (\d+)", text).group(1))
+    assert B.status_str(B.SPEC_OK) == "ok"
+    for st in range(1, 5):
+        assert B.status_str(st) not in ("ok", "unknown status")
+    assert B.status_str(99) == "unknown status"
+
+
+FAKE = 1 << 20      # a 256-aligned fake device address; never dereferenced on these paths
+
+
+def _attn(**kw):
+    a = B.SpecAttnArgs()
+    a.num_q_heads, a.num_kv_heads, a.head_dim, a.dtype = 8, 2, 128, B.SPEC_BF16
+    a.q = a.k = a.v = a.out = FAKE
+    a.q_stride_tok, a.q_stride_head = 8 * 128, 128
+    a.kv_stride_tok, a.kv_stride_head = 2 * 128, 128
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+def _acc(**kw):
+    a = B.SpecAcceptArgs()
+    a.vocab, a.dtype = 1000, B.SPEC_F32
+    a.target_logits = a.draft_probs = a.draft_tokens = a.uniforms = FAKE
+    a.accepted_len = a.next_token = FAKE
+    a.logits_stride = a.probs_stride = 1000
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+def _req(ctx=(5, 9), k=(2, 3), parent=None):
+    return B.make_requests(np.array(ctx), None if parent is not None else np.array(k), parent)
+
+
+def _ws(req, attn, acc):
+    return B.spec_workspace_bytes(req, attn, acc)
+
+
+def test_workspace_bytes_valid(lib):
+    st, dev, host = _ws(_req(), _attn(), _acc())
+    assert st == B.SPEC_OK and dev > 0 and host > 0 and dev % 256 == 0 and host <= dev
+    # attention-only and acceptance-only need no more than the whole step
+    st_a, dev_a, _ = _ws(_req(), _attn(), None)
+    st_c, dev_c, _ = _ws(_req(), None, _acc())
+    assert st_a == st_c == B.SPEC_OK and dev_a <= dev and dev_c <= dev
+    # deterministic
+    assert _ws(_req(), _attn(), _acc()) == (st, dev, host)
+    # a forced split changes the partial area, not the verdict
+    st2, dev2, _ = _ws(_req(ctx=(3000, 5000)), _attn(split_kv=256), None)
+    st3, dev3, _ = _ws(_req(ctx=(3000, 5000)), _attn(split_kv=8192), None)
+    assert st2 == st3 == B.SPEC_OK and dev2 > dev3
+
+
+@pytest.mark.parametrize("req,expect", [
+    (dict(ctx=(5, -1)), B.SPEC_ERR_INVALID_ARG),
+    (dict(k=(2, 17)), B.SPEC_ERR_INVALID_ARG),
+    (dict(k=(-1, 2)), B.SPEC_ERR_INVALID_ARG),
+    (dict(k=(0, 16)), B.SPEC_OK),
+    (dict(parent=[0, 0, 1]), B.SPEC_ERR_INVALID_ARG),
+    (dict(parent=[-1, 0, 2]), B.SPEC_ERR_INVALID_ARG),
+    (dict(parent=[-1, 0, 0, 1]), B.SPEC_OK),
+    (dict(parent=[-1] + list(range(32))), B.SPEC_ERR_INVALID_ARG),      # 33 nodes
+])
+def test_request_checks(lib, req, expect):
+    assert _ws(_req(**req), _attn(), _acc())[0] == expect
+
+
+def test_null_and_empty_requests(lib):
+    dev, host = C.c_size_t(0), C.c_size_t(0)
+    assert lib.spec_workspace_bytes(None, None, None, C.byref(dev), C.byref(host)) == B.SPEC_ERR_INVALID_ARG
+    r = B.make_requests(np.zeros(0, np.int32), np.zeros(0, np.int32))
+    assert _ws(r, _attn(), None)[0] == B.SPEC_ERR_INVALID_ARG
+    r = _req()
+    r.draft_len = C.POINTER(C.c_int32)()        # chain mode needs draft lengths
+    assert _ws(r, _attn(), None)[0] == B.SPEC_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(num_q_heads=6, num_kv_heads=4), B.SPEC_ERR_INVALID_ARG),
+    (dict(num_kv_heads=0), B.SPEC_ERR_INVALID_ARG),
+    (dict(head_dim=96), B.SPEC_ERR_UNSUPPORTED),
+    (dict(head_dim=64, q_stride_tok=8 * 64, q_stride_head=64, kv_stride_tok=128, kv_stride_head=64), B.SPEC_OK),
+    (dict(dtype=7), B.SPEC_ERR_INVALID_ARG),
+    (dict(q=None), B.SPEC_ERR_INVALID_ARG),
+    (dict(out=None), B.SPEC_ERR_INVALID_ARG),
+    (dict(k=FAKE + 2), B.SPEC_ERR_INVALID_ARG),             # misaligned
+    (dict(kv_stride_tok=2 * 128 + 4), B.SPEC_ERR_INVALID_ARG),   # bf16 rows must stay 16-byte aligned
+    (dict(q_stride_head=0), B.SPEC_ERR_INVALID_ARG),
+    (dict(split_kv=33), B.SPEC_ERR_INVALID_ARG),
+    (dict(split_kv=-32), B.SPEC_ERR_INVALID_ARG),
+    (dict(split_kv=64), B.SPEC_OK),
+    (dict(dtype=B.SPEC_F32, kv_stride_tok=2 * 128 + 4), B.SPEC_OK),
+])
+def test_attention_checks(lib, kw, expect):
+    assert _ws(_req(), _attn(**kw), None)[0] == expect
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(vocab=0), B.SPEC_ERR_INVALID_ARG),
+    (dict(vocab=4096 * 1024 + 1, logits_stride=4096 * 1024 + 4, probs_stride=4096 * 1024 + 4),
+     B.SPEC_ERR_INVALID_ARG),
+    (dict(uniforms=None), B.SPEC_ERR_INVALID_ARG),
+    (dict(next_token=None), B.SPEC_ERR_INVALID_ARG),
+    (dict(draft_tokens=None), B.SPEC_ERR_INVALID_ARG),
+    (dict(logits_stride=999), B.SPEC_ERR_INVALID_ARG),
+    (dict(logits_stride=1002), B.SPEC_ERR_INVALID_ARG),      # fp32 rows must stay 16-byte aligned
+    (dict(dtype=B.SPEC_BF16, logits_stride=1004, probs_stride=1008), B.SPEC_ERR_INVALID_ARG),
+    (dict(dtype=B.SPEC_BF16, logits_stride=1008, probs_stride=1008), B.SPEC_OK),
+    (dict(target_logits=FAKE + 4), B.SPEC_ERR_INVALID_ARG),
+    (dict(dtype=3), B.SPEC_ERR_INVALID_ARG),
+])
+def test_accept_checks(lib, kw, expect):
+    assert _ws(_req(), None, _acc(**kw))[0] == expect
+
+
+def test_all_plain_decoding_needs_no_draft_arrays(lib):
+    r = _req(k=(0, 0))
+    assert _ws(r, None, _acc(draft_probs=None, draft_tokens=None))[0] == B.SPEC_OK
+
+
+def test_entry_points_reject_before_any_device_work(lib):
+    req, attn, acc = _req(), _attn(), _acc()
+    st, dev, host = _ws(req, attn, acc)
+    staging = np.full(host + 64, 0xAB, dtype=np.uint8)
+    sp = staging.ctypes.data
+    # workspace too small / misaligned / missing; staging too small: nothing is written
+    assert B.spec_verify(req, attn, acc, FAKE, dev - 256, sp, host, None) == B.SPEC_ERR_WORKSPACE
+    assert B.spec_verify(req, attn, acc, FAKE + 64, dev, sp, host, None) == B.SPEC_ERR_WORKSPACE
+    assert B.spec_verify(req, attn, acc, 0, dev, sp, host, None) == B.SPEC_ERR_WORKSPACE
+    assert B.spec_verify(req, attn, acc, FAKE, dev, sp, host - 1, None) == B.SPEC_ERR_WORKSPACE
+    assert B.spec_verify(req, attn, acc, FAKE, dev, 0, host, None) == B.SPEC_ERR_WORKSPACE
+    assert (staging == 0xAB).all()
+    # missing argument blocks
+    assert B.spec_verify(req, None, acc, FAKE, dev, sp, host, None) == B.SPEC_ERR_INVALID_ARG
+    assert B.spec_verify(req, attn, None, FAKE, dev, sp, host, None) == B.SPEC_ERR_INVALID_ARG
+    assert B.spec_verify_attn(req, None, FAKE, dev, sp, host, None) == B.SPEC_ERR_INVALID_ARG
+    assert B.spec_accept(req, None, FAKE, dev, sp, host, None) == B.SPEC_ERR_INVALID_ARG
+    # invalid arguments reported by the entry points themselves
+    assert B.spec_verify_attn(req, _attn(head_dim=32), FAKE, dev, sp, host, None) == B.SPEC_ERR_UNSUPPORTED
+    assert B.spec_accept(_req(k=(1, 99)), acc, FAKE, dev, sp, host, None) == B.SPEC_ERR_INVALID_ARG
+    assert (staging == 0xAB).all()
+
+
+def test_workspace_grows_with_work(lib):
+    a = _ws(_req(ctx=(100, 100)), _attn(), _acc())
+    b = _ws(_req(ctx=(100, 100, 100, 100), k=(2, 3, 4, 5)), _attn(), _acc())
+    c = _ws(_req(), _attn(), _acc(vocab=128256, logits_stride=128256, probs_stride=128256))
+    assert a[1] <= b[1] and _ws(_req(), _attn(), _acc())[1] < c[1]

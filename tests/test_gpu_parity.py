@@ -1,0 +1,202 @@
+"""GPU parity: the HIP verify path against the fp64 oracle on the same seeded inputs.
+
+Every call goes through the C ABI (spec_verify / spec_verify_attn / spec_accept).
+Tolerances are stated in parity_util: attention row-relative <= 2e-3;
+accepted lengths, nodes and next tokens bit-exact except counted near ties.
+"""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import parity_util as U
+from paper_2505_17074_amd import workload as W
+from paper_2505_17074_amd.batch import DeviceBatch, Verifier
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+def _run(pool, which="verify", split_kv=0):
+    b = DeviceBatch(pool, "cuda")
+    v = Verifier(b, split_kv=split_kv)
+    v.run(which)
+    return v.results()
+
+
+def _check(pool, res, attn_reqs=None, accept=True, tag=""):
+    if attn_reqs is None:
+        attn_reqs = range(pool.batch)
+    if len(attn_reqs):
+        ref = U.oracle_attention_rows(pool, attn_reqs)
+        r = U.attention_ratios(res["out"], pool, ref)
+        print(f"{tag} attention rows={r.size} worst={r.max():.3e} over1e-3={np.mean(r > 1e-3):.4f}", flush=True)
+        assert np.isfinite(r).all() and r.max() <= U.ATTN_RTOL, tag
+    if accept:
+        ref = U.oracle_accept(pool)
+        bad, ties = U.compare_accept(res, ref, pool)
+        acc = res["accepted_len"]
+        print(f"{tag} accept B={pool.batch} mean_accepted={acc.mean():.3f} near_ties={ties} mismatches={bad}",
+              flush=True)
+        assert not bad, (tag, bad)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_tiny_f32(gpu_lib, seed):
+    _say(f"tiny_f32 seed={seed}")
+    pool = W.make_pool(W.CONFIGS[0], seed)
+    _check(pool, _run(pool), tag=f"tiny_f32/{seed}")
+
+
+REDUCED = {1: 6, 2: 24, 3: 2, 4: 6}
+
+
+@pytest.mark.parametrize("idx,seed", [(i, s) for i in (1, 2, 3, 4) for s in (0, 1)])
+def test_reduced_batches(gpu_lib, idx, seed):
+    cfg = W.CONFIGS[idx]
+    _say(f"{cfg.name} batch={REDUCED[idx]} seed={seed}")
+    pool = W.make_pool(cfg, seed, batch=REDUCED[idx])
+    _check(pool, _run(pool), tag=f"{cfg.name}/b{REDUCED[idx]}/{seed}")
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4])
+def test_full_size_sampled(gpu_lib, idx):
+    """Full-size workloads in the benchmark's launch configuration: attention on
+    sampled requests (first, middle, last), acceptance on every request."""
+    cfg = W.CONFIGS[idx]
+    _say(f"{cfg.name} full size")
+    pool = W.make_pool(cfg, 0)
+    res = _run(pool)
+    B = pool.batch
+    _check(pool, res, attn_reqs=sorted({0, B // 2, B - 1}), tag=f"{cfg.name}/full")
+    torch.cuda.empty_cache()
+
+
+def test_split_invariance(gpu_lib):
+    pool = W.make_pool(W.CONFIGS[1], 3, batch=4)
+    outs = {}
+    for split in (32, 96, 512, 0, 1 << 16):
+        _say(f"split_kv={split}")
+        res = _run(pool, split_kv=split)
+        _check(pool, res, accept=(split == 0), tag=f"split{split}")
+        outs[split] = res
+    base = outs[0]
+    for split, res in outs.items():
+        np.testing.assert_allclose(res["out"], base["out"], rtol=0, atol=5e-3 * np.abs(base["out"]).max())
+
+
+def test_deterministic(gpu_lib):
+    _say("determinism ragged_gqa b32")
+    pool = W.make_pool(W.CONFIGS[2], 5, batch=32)
+    b = DeviceBatch(pool, "cuda")
+    v = Verifier(b)
+    v.run()
+    first = v.results()
+    for _ in range(3):
+        v.run()
+    second = v.results()
+    for key in first:
+        assert np.array_equal(first[key], second[key]), key
+
+
+EDGE = [
+    ("ctx_edges_k0_k16", dict(ctx=[0, 1, 31, 32, 33, 100], k=[0, 1, 16, 4, 0, 7])),
+    ("d64_mha", dict(ctx=[17, 300, 64], k=[3, 0, 8], Hq=4, Hkv=4, d=64)),
+    ("f32_valu_gqa_d128", dict(ctx=[5, 130, 70], k=[2, 6, 0], Hq=8, Hkv=2, d=128, qkv=W.F32)),
+    ("f32_valu_d64", dict(ctx=[200, 0], k=[16, 3], Hq=2, Hkv=1, d=64, qkv=W.F32)),
+    ("tree_nonbinary", dict(ctx=[0, 50, 300], tree_parent=[-1, 0, 0, 0, 1, 1, 2, 4, 4, 7])),
+    ("wide_group_split", dict(ctx=[90, 40], k=[16, 9], Hq=32, Hkv=2)),
+    ("vocab_5000_bf16_logits", dict(ctx=[10, 20, 30, 40], k=[4, 3, 2, 1], V=5000, logit=W.BF16)),
+    ("vocab_tail_f32", dict(ctx=[10, 20], k=[4, 8], V=4100)),
+    ("long_single", dict(ctx=[20000], k=[5])),
+]
+
+
+@pytest.mark.parametrize("name,kw", EDGE, ids=[e[0] for e in EDGE])
+def test_edge_cases(gpu_lib, name, kw):
+    _say(name)
+    pool = U.custom_pool(**kw, seed=hash(name) % 1000)
+    _check(pool, _run(pool), tag=name)
+
+
+def test_custom_scale_and_strided_query(gpu_lib):
+    _say("custom scale, head-major query layout")
+    pool = U.custom_pool(ctx=[40, 77], k=[3, 5], Hq=8, Hkv=2)
+    b = DeviceBatch(pool, "cuda")
+    # store Q head-major ([Hq, Nq, d]) and pass its strides
+    qhm = b.q.permute(1, 0, 2).contiguous()
+    b.q = qhm.permute(1, 0, 2)
+    v = Verifier(b)
+    v.attn.q = b.q.data_ptr()
+    v.attn.q_stride_tok, v.attn.q_stride_head = b.q.stride(0), b.q.stride(1)
+    v.attn.scale = 0.05
+    v.run("attn")
+    res = v.results()
+    from oracle import verify_attention
+    ref = verify_attention(pool.q, pool.k, pool.v, pool.ctx_len, pool.n_q, 2, dtype=pool.qkv_dtype, scale=0.05)
+    r = np.abs(res["out"] - ref).max(-1) / np.abs(ref).max(-1)
+    assert r.max() <= U.ATTN_RTOL
+
+
+def test_p_equals_q_accepts_every_draft(gpu_lib):
+    _say("p == q")
+    pool = U.custom_pool(ctx=[3] * 8, k=[1, 2, 3, 4, 5, 6, 7, 8], V=2048)
+    # draft rows := the target softmax (fp32), uniforms kept below 0.99
+    lg = pool.target_logits.astype(np.float64)
+    q0, d0 = pool.q_start, pool.d_start
+    for i in range(pool.batch):
+        for j in range(int(pool.draft_len[i])):
+            row = lg[q0[i] + j]
+            e = np.exp(row - row.max())
+            pool.draft_probs[d0[i] + j] = (e / e.sum()).astype(np.float32)
+    pool.uniforms[:] = np.minimum(pool.uniforms, np.float32(0.99))
+    res = _run(pool, "accept")
+    assert np.array_equal(res["accepted_len"], pool.draft_len)
+
+
+def _cells(breaks):
+    b = sorted(set([0.0, 1.0] + [float(x) for x in breaks if 0.0 < x < 1.0]))
+    return [((lo + hi) / 2.0, hi - lo) for lo, hi in zip(b[:-1], b[1:])]
+
+
+def test_emitted_token_distribution_exact_on_gpu(gpu_lib):
+    """The vocab-8 identity, black-box through the GPU kernels: one request per
+    uniform cell; summing cell probabilities by the GPU's outcomes must give
+    the target distribution exactly (every midpoint is far from a boundary)."""
+    _say("vocab-8 enumeration through the GPU")
+    V = 8
+    rng = np.random.default_rng(17)
+    p0 = rng.random(V) ** 2 + 0.01
+    p0 /= p0.sum()
+    p1 = rng.random(V) + 0.01
+    p1 /= p1.sum()
+    q0 = rng.random(V) + 0.01
+    q0 /= q0.sum()
+    q0 = q0.astype(np.float32).astype(np.float64)
+    q0 /= q0.sum()
+    q0 = q0.astype(np.float32)
+    qd = q0.astype(np.float64)
+    res = np.maximum(0, p0 - qd)
+    fin = []
+    for w in (res, p1):
+        fin.extend(np.cumsum(w) / w.sum())
+    cases = []
+    for x in range(V):
+        for (u0, l0), (u1, l1) in itertools.product(_cells([min(1.0, p0[x] / qd[x])]), _cells(fin)):
+            cases.append((x, np.float32(u0), np.float32(u1), qd[x] * l0 * l1))
+    n = len(cases)
+    pool = U.custom_pool(ctx=[0] * n, k=[1] * n, Hq=1, Hkv=1, d=64, V=V)
+    pool.target_logits[:] = np.tile(np.log(np.stack([p0, p1])).astype(np.float32), (n, 1))
+    pool.draft_probs[:] = np.tile(q0[None], (n, 1))
+    pool.draft_tokens[:] = [c[0] for c in cases]
+    pool.uniforms[:] = np.array([[c[1], c[2]] for c in cases], np.float32).ravel()
+    out = _run(pool, "accept")
+    dist = np.zeros(V)
+    for i, (x, _, _, w) in enumerate(cases):
+        y = x if out["accepted_len"][i] == 1 else out["next_token"][i]
+        dist[y] += w
+    np.testing.assert_allclose(dist, p0, rtol=0, atol=1e-6)
