@@ -186,8 +186,9 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
     int rows_max = 1;
     for (int i = 0; i < P.B; ++i) {
       const int n = P.reqs[i].nq;
-      const int ng = (G * n + rmax - 1) / rmax;
-      hpg[i] = (G + ng - 1) / ng;
+      const int hmax = std::max(1, rmax / n);          // heads that fit one item
+      const int ng = (G + hmax - 1) / hmax;
+      hpg[i] = (G + ng - 1) / ng;                      // balanced, still <= hmax
       groups[i] = (G + hpg[i] - 1) / hpg[i];
       streams += ((int64_t)P.reqs[i].ctx + n) * Hkv * groups[i];
       rows_max = std::max(rows_max, hpg[i] * n);
