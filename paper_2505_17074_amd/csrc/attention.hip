@@ -34,184 +34,334 @@ __device__ __forceinline__ bool visible(int t, int ctx, uint32_t anc) {
 }
 
 // ---------------------------------------------------------------------------
-// bf16 MFMA path.  One wave per work item, all query rows of the item in NR
-// tiles of 16.  Per 32-key tile:
-//   S^T[key, row] = K[key, :] . Q[row, :]      v_mfma_f32_16x16x32_bf16, K as A
+// bf16 MFMA path.  One work-group of W waves per work item; wave w owns query
+// rows 16w .. 16w+15 of the item (W = row tiles).  The waves share 32-key K
+// and V tiles that stream HBM -> LDS through an NS-stage ring of direct
+// global_load_lds_dwordx4 transfers (no register staging).  Every transfer
+// reads whole key rows with consecutive lanes and lands in LDS in lane order;
+// the 16-byte chunks of row r are XOR-swizzled (swk for K, swv for V) so that
+// both reads below are bank-conflict free and every lane's read addresses
+// are one per-lane base plus compile-time offsets.  Per tile and wave:
+//   S^T[key, row] = K[key, :] . Q[row, :]   v_mfma_f32_16x16x32_bf16, K as A
+//                                            (A rows: ds_read_b128)
 //   online softmax over keys (fp32, log2 domain)
-//   O^T[e, row]  += V^T[e, key] . P^T[key, row] with P = hi + lo in two bf16
-//                   parts, so P's rounding stays near fp32 (error ~2^-17)
+//   O^T[e, row]  += V^T[e, key] . P^T[key, row]   with P = hi + lo in two
+//                   bf16 parts, so P's rounding stays near fp32 (~2^-17)
 // The 16 MFMA A-rows of key tile kt hold keys 8*(m>>2) + 4*kt + (m&3): the
 // C layout then leaves lane group g holding keys 8g..8g+7 of its query row,
-// which is exactly the B operand the PV product needs, with no data movement.
-// V is staged through a wave-private LDS tile and read back transposed
-// (8 keys of one column per lane).
+// which is exactly the B operand of the PV product, with no data movement.
+// The V^T A operand comes from two ds_read_b64_tr_b16 per 16 columns: in a
+// 16-lane group, lane i receives element i&3 of source lane 4j + (i>>2) as
+// its element j, so source lane s pointing at key row 8g + 4h + (s>>2),
+// columns 16e + 4(s&3) .. +3 hands lane i the keys 8g + 4h + 0..3 of column
+// 16e + i.  The item's output is staged through LDS and written as rows.
 // ---------------------------------------------------------------------------
-template <int D, int NR>
-__global__ __launch_bounds__(64) void attn_split_mfma(AttnParams p) {
-  constexpr int KS = D / 32;       // QK k-steps
-  constexpr int ET = D / 16;       // PV column tiles
-  constexpr int VCH = D / 16;      // 16-byte V chunks per lane per tile
-  constexpr int PITCH = D + 2;     // LDS row pitch (bf16): odd dword count, conflict-free columns
-  __shared__ uint16_t vt[32 * PITCH];
+typedef __attribute__((address_space(3))) void lds_void_t;
+#ifndef SV_NS1
+#define SV_NS1 3
+#endif
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
 
-  const int lane = threadIdx.x;
+template <int D>
+struct Geo {
+  static constexpr int CH = D / 8;                  // 16-byte chunks per row
+  static constexpr int RPI = 64 / CH;               // rows per 1 KB transfer
+  static constexpr int IPM = 32 / RPI;              // transfers per 32-row matrix
+  static constexpr int ROWB = D * 2;                // bytes of one LDS row
+  static constexpr int MAT = 32 * ROWB;             // bytes of one K (or V) tile
+  static constexpr int STAGE = 2 * MAT;
+};
+
+// K rows: distinct over the 16 rows of one quarter-wave A read.
+template <int D>
+__device__ __forceinline__ int swk(int r) {
+  if constexpr (D == 128) return (r & 3) | (((r >> 3) & 3) << 2);
+  else return ((r >> 1) & 1) | (((r >> 3) & 3) << 1);
+}
+// V rows: even (keeps 32-byte column pairs together), distinct pair slots over
+// the 8 rows of one half-wave transpose read.
+template <int D>
+__device__ __forceinline__ int swv(int r) {
+  if constexpr (D == 128) return 2 * ((r & 3) | (((r >> 3) & 1) << 2));
+  else return 2 * (((r >> 1) & 1) | (((r >> 3) & 1) << 1));
+}
+
+// vmcnt(n) for gfx950 (expcnt and lgkmcnt left at "no wait")
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+template <int D, int W>
+struct Xfer {
+  static constexpr int NI = 2 * Geo<D>::IPM;        // transfers per tile (K then V)
+  static constexpr int PER = (NI + W - 1) / W;      // per wave (padded with repeats)
+};
+
+// Byte offset, inside a tile, of the global chunk lane `lane` moves in
+// transfer j (tile row row_in_tile * row_bytes + swizzled chunk).
+template <int D>
+__device__ __forceinline__ uint32_t xfer_offset(int j, int lane, int row_bytes, int* row_in_tile) {
+  using G = Geo<D>;
+  const bool isv = j >= G::IPM;
+  const int jj = isv ? j - G::IPM : j;
+  const int row = jj * G::RPI + lane / G::CH;
+  const int chunk = (lane % G::CH) ^ (isv ? swv<D>(row) : swk<D>(row));
+  *row_in_tile = row;
+  return (uint32_t)row * (uint32_t)row_bytes + (uint32_t)chunk * 16u;
+}
+
+template <int D, int W>
+struct XferPlan {
+  uint32_t off[Xfer<D, W>::PER];    // per-lane byte offset inside the tile
+};
+
+// Wave w's transfers of the tile starting at key t0 into `stage`, as
+// buffer_load_dwordx4 ... lds with the tile start in soffset and each lane's
+// precomputed offset in voffset.  Tiles that reach past ke clamp their rows
+// to ke - 1 (in bounds, masked later); the pad transfers of uneven splits
+// repeat an earlier one with identical data.
+template <int D, int W>
+__device__ __forceinline__ void issue_tile(char* stage, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
+                                           int row_bytes, int t0, int ke, int w, int lane,
+                                           const XferPlan<D, W>& X) {
+  using G = Geo<D>;
+  if (t0 + 32 <= ke) {                // wave-uniform: the whole tile is inside the item
+    const uint32_t soff = (uint32_t)t0 * (uint32_t)row_bytes;
+#pragma unroll
+    for (int q = 0; q < Xfer<D, W>::PER; ++q) {
+      const int j = (w + q * W) % Xfer<D, W>::NI;
+      const bool isv = j >= G::IPM;
+      const int jj = isv ? j - G::IPM : j;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(isv ? rv : rk, (lds_void_t*)(stage + (isv ? G::MAT : 0) + jj * 1024),
+                                               16, X.off[q], soff, 0, 0);
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < Xfer<D, W>::PER; ++q) {
+      const int j = (w + q * W) % Xfer<D, W>::NI;
+      const bool isv = j >= G::IPM;
+      const int jj = isv ? j - G::IPM : j;
+      int row;
+      const uint32_t full = xfer_offset<D>(j, lane, row_bytes, &row);
+      const uint32_t chunk_bytes = full - (uint32_t)row * (uint32_t)row_bytes;
+      const int key = min(t0 + row, ke - 1);       // >= kb >= 0: items are never empty
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(isv ? rv : rk, (lds_void_t*)(stage + (isv ? G::MAT : 0) + jj * 1024),
+                                               16, (uint32_t)key * (uint32_t)row_bytes + chunk_bytes, 0u, 0, 0);
+    }
+  }
+}
+
+template <int D>
+struct RowTile {
+  bf16x8 q[D / 32];
+  f32x4 o[D / 16];
+  uint32_t koff[D / 32];   // A-row read offsets (key tile 0; tile 1 is +4 rows)
+  uint32_t voff[D / 16];   // transpose-read offsets (keys 8g + 0..3; +4 rows for 4..7)
+  uint32_t anc;
+  float m, l;
+};
+
+template <int D>
+__device__ __forceinline__ void compute_tile(const char* stage, RowTile<D>& S, int t0, int ke, int ctx,
+                                             float scale_log2, int lane) {
+  using G = Geo<D>;
+  constexpr int KS = D / 32, ET = D / 16;
+  const int grp = lane >> 4;
+  f32x4 s[2];
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 kop = *reinterpret_cast<const bf16x8*>(stage + S.koff[ks] + kt * 4 * G::ROWB);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, S.q[ks], acc, 0, 0, 0);
+    }
+    s[kt] = acc;
+  }
+  // Scores in log2 units.  The exponent reference S.m trails the running max
+  // by at most kLazy: it moves (and O, l are rescaled) only when a score
+  // exceeds it by more than that, so p <= 2^kLazy and the common tile leaves
+  // the accumulators to the matrix cores alone.
+  constexpr float kLazy = 8.f;
+  float sv[8];
+  bool need = false;
+  if (t0 + 32 <= min(ke, ctx)) {      // wave-uniform: every key visible to every row
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      sv[x] = s[x >> 2][x & 3] * scale_log2;
+      need |= sv[x] > S.m + kLazy;
+    }
+  } else {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = t0 + 8 * grp + 4 * kt + i;
+        float x = s[kt][i] * scale_log2;
+        if (t >= ke || !visible(t, ctx, S.anc)) x = -INFINITY;
+        sv[kt * 4 + i] = x;
+        need |= x > S.m + kLazy;
+      }
+    }
+  }
+  if (__any(need)) {                  // wave-uniform
+    float mloc = sv[0];
+#pragma unroll
+    for (int x = 1; x < 8; ++x) mloc = fmaxf(mloc, sv[x]);
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    const float m_new = fmaxf(S.m, mloc);
+    const float alpha = (m_new == S.m) ? 1.f : exp2f(S.m - m_new);    // S.m = -inf gives 0
+    S.l *= alpha;
+#pragma unroll
+    for (int et = 0; et < ET; ++et) S.o[et] *= alpha;
+    S.m = m_new;
+  }
+  const float m_use = (S.m == -INFINITY) ? 0.f : S.m;
+  float psum = 0.f;
+  bf16x8 phi, plo;
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    const float pv = exp2f(sv[x] - m_use);
+    psum += pv;
+    const __bf16 h = static_cast<__bf16>(pv);
+    phi[x] = h;
+    plo[x] = static_cast<__bf16>(pv - static_cast<float>(h));
+  }
+  S.l += psum;
+  const char* vbase = stage + G::MAT;
+#pragma unroll
+  for (int et = 0; et < ET; ++et) {
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vbase + S.voff[et]));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vbase + S.voff[et] + 4 * G::ROWB));
+    const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    S.o[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, phi, S.o[et], 0, 0, 0);
+    S.o[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, plo, S.o[et], 0, 0, 0);
+  }
+}
+
+template <int D, int W, int NS>
+struct AttnLds {
+  static constexpr int RING = NS * Geo<D>::STAGE;
+  static constexpr int OUT = W * 16 * (D + 4) * 4;  // fp32 output staging, padded rows
+  static constexpr int BYTES = RING > OUT ? RING : OUT;
+};
+
+template <int D, int W, int NS>
+__global__ __launch_bounds__(64 * W) void attn_split_mfma(AttnParams p) {
+  using G = Geo<D>;
+  constexpr int ET = D / 16, KS = D / 32;
+  constexpr int PER = Xfer<D, W>::PER;
+  static_assert(NS >= 2, "ring depth");
+  __shared__ __attribute__((aligned(1024))) char lds[AttnLds<D, W, NS>::BYTES];
+
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c16 = lane & 15, grp = lane >> 4;
   const AttnItem it = p.items[blockIdx.x];
   const ReqInfo rq = p.reqs[it.req];
   const int n = rq.nq;
   const int R = it.nheads * n;
   const int ctx = rq.ctx;
-  const uint16_t* __restrict__ Kb =
-      static_cast<const uint16_t*>(p.k) + (int64_t)rq.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh;
-  const uint16_t* __restrict__ Vb =
-      static_cast<const uint16_t*>(p.v) + (int64_t)rq.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh;
+  const int row_bytes = (int)(p.kv_st * 2);
+  const char* Kb = static_cast<const char*>(p.k) + ((int64_t)rq.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh) * 2;
+  const char* Vb = static_cast<const char*>(p.v) + ((int64_t)rq.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh) * 2;
+  const int ntiles = (it.ke - it.kb + 31) / 32;
+  // byte range of this request's rows for this KV head (the host keeps it < 2^31)
+  const int range = (rq.ctx + rq.nq) * row_bytes;
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)Kb, 0, range, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)Vb, 0, range, 0x00020000);
 
-  bf16x8 qop[NR][KS];
-  uint32_t anc[NR];
+  XferPlan<D, W> X;
 #pragma unroll
-  for (int rt = 0; rt < NR; ++rt) {
-    const int r = rt * 16 + c16;
+  for (int q = 0; q < PER; ++q) {
+    int row;
+    X.off[q] = xfer_offset<D>((w + q * W) % Xfer<D, W>::NI, lane, row_bytes, &row);
+  }
+
+  RowTile<D> S;
+  {
+    const int r = w * 16 + c16;
     if (r < R) {
       const int hh = r / n, j = r - hh * n;
       const uint16_t* qp = static_cast<const uint16_t*>(p.q) + (int64_t)(rq.q0 + j) * p.q_st +
                            (int64_t)(it.head_lo + hh) * p.q_sh + grp * 8;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) qop[rt][ks] = *reinterpret_cast<const bf16x8*>(qp + ks * 32);
-      anc[rt] = p.topo->anc[j];
+      for (int ks = 0; ks < KS; ++ks) S.q[ks] = *reinterpret_cast<const bf16x8*>(qp + ks * 32);
+      S.anc = p.topo->anc[j];
     } else {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) qop[rt][ks] = bf16x8{};
-      anc[rt] = 0u;
+      for (int ks = 0; ks < KS; ++ks) S.q[ks] = bf16x8{};
+      S.anc = 0u;
+    }
+    S.m = -INFINITY;
+    S.l = 0.f;
+#pragma unroll
+    for (int et = 0; et < ET; ++et) S.o[et] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int rk = 8 * (c16 >> 2) + (c16 & 3);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) S.koff[ks] = rk * G::ROWB + (((ks * 4 + grp) ^ swk<D>(rk)) * 16);
+    const int rv = 8 * grp + (c16 >> 2);
+#pragma unroll
+    for (int et = 0; et < ET; ++et)
+      S.voff[et] = rv * G::ROWB + (((2 * et + ((c16 & 3) >> 1)) ^ swv<D>(rv)) * 16) + (c16 & 1) * 8;
+  }
+  const bool active = w * 16 < R;     // wave-uniform: this wave has query rows
+
+  // the ring's first NS-1 tiles go out after the query loads
+#pragma unroll
+  for (int st = 0; st < NS - 1; ++st)
+    issue_tile<D, W>(lds + st * G::STAGE, rk, rv, row_bytes, it.kb + 32 * st, it.ke, w, lane, X);
+
+  for (int tb = 0; tb < ntiles; tb += NS) {
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {           // stage index is a compile-time constant
+      const int t = tb + st;
+      if (t >= ntiles) break;
+      wait_vm<PER * (NS - 2)>();      // this wave's transfers of tile t have landed
+      __syncthreads();                // ... and everyone's; stage (t-1) % NS is free
+      issue_tile<D, W>(lds + ((st + NS - 1) % NS) * G::STAGE, rk, rv, row_bytes, it.kb + 32 * (t + NS - 1), it.ke,
+                       w, lane, X);
+      if (active) compute_tile<D>(lds + st * G::STAGE, S, it.kb + 32 * t, it.ke, ctx, p.scale_log2, lane);
     }
   }
+  wait_vm<0>();
+  __syncthreads();                    // ring no longer read: reuse it for the output
 
-  f32x4 o[NR][ET];
-  float m_run[NR], l_run[NR];
+  // row sums across the four lane groups; stage O^T into row-major LDS
+  float l = S.l;
+  l += __shfl_xor(l, 16);
+  l += __shfl_xor(l, 32);
+  float* ost = reinterpret_cast<float*>(lds) + w * 16 * (D + 4);
+  const float scale = it.seg < 0 ? 1.f / l : 1.f;
 #pragma unroll
-  for (int rt = 0; rt < NR; ++rt) {
-    m_run[rt] = -INFINITY;
-    l_run[rt] = 0.f;
-#pragma unroll
-    for (int et = 0; et < ET; ++et) o[rt][et] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int et = 0; et < ET; ++et) {
+    const f32x4 v = S.o[et] * scale;
+    *reinterpret_cast<float4*>(ost + c16 * (D + 4) + et * 16 + 4 * grp) = make_float4(v[0], v[1], v[2], v[3]);
   }
-  const int nrt = (R + 15) >> 4;   // active row tiles (wave-uniform)
-
-  for (int t0 = it.kb; t0 < it.ke; t0 += 32) {
-    // K operands straight from HBM in MFMA A layout (16 B per lane per k-step)
-    bf16x8 kop[2][KS];
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      const int key = min(t0 + 8 * (c16 >> 2) + 4 * kt + (c16 & 3), it.ke - 1);
-      const uint16_t* kp = Kb + (int64_t)key * p.kv_st + grp * 8;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kop[kt][ks] = *reinterpret_cast<const bf16x8*>(kp + ks * 32);
-    }
-    // V tile, coalesced: consecutive lanes read consecutive 16 B of a key row
-    uint4 vraw[VCH];
-#pragma unroll
-    for (int c = 0; c < VCH; ++c) {
-      const int chunk = c * 64 + lane;
-      const int key = min(t0 + chunk / (D / 8), it.ke - 1);
-      vraw[c] = *reinterpret_cast<const uint4*>(Vb + (int64_t)key * p.kv_st + (chunk % (D / 8)) * 8);
-    }
-    __syncthreads();   // previous tile's transposed reads are done
-#pragma unroll
-    for (int c = 0; c < VCH; ++c) {
-      const int chunk = c * 64 + lane;
-      uint32_t* dst = reinterpret_cast<uint32_t*>(vt + (chunk / (D / 8)) * PITCH + (chunk % (D / 8)) * 8);
-      dst[0] = vraw[c].x;
-      dst[1] = vraw[c].y;
-      dst[2] = vraw[c].z;
-      dst[3] = vraw[c].w;
-    }
-    __syncthreads();
-    bf16x8 vop[ET];
-#pragma unroll
-    for (int et = 0; et < ET; ++et) {
-#pragma unroll
-      for (int m = 0; m < 8; ++m) {
-        const uint16_t bits = vt[(8 * grp + m) * PITCH + et * 16 + c16];
-        vop[et][m] = __builtin_bit_cast(__bf16, bits);
-      }
-    }
-
-#pragma unroll
-    for (int rt = 0; rt < NR; ++rt) {
-      if (rt >= nrt) break;
-      f32x4 s[2];
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop[kt][ks], qop[rt][ks], acc, 0, 0, 0);
-        s[kt] = acc;
-      }
-      float sv[8];
-      float mloc = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int t = t0 + 8 * grp + 4 * kt + i;
-          float x = s[kt][i] * p.scale_log2;
-          if (t >= it.ke || !visible(t, ctx, anc[rt])) x = -INFINITY;
-          sv[kt * 4 + i] = x;
-          mloc = fmaxf(mloc, x);
-        }
-      }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-      const float m_new = fmaxf(m_run[rt], mloc);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = exp2f(m_run[rt] - m_use);
-      float psum = 0.f;
-      bf16x8 phi, plo;
-#pragma unroll
-      for (int x = 0; x < 8; ++x) {
-        const float pv = exp2f(sv[x] - m_use);
-        psum += pv;
-        const __bf16 h = static_cast<__bf16>(pv);
-        phi[x] = h;
-        plo[x] = static_cast<__bf16>(pv - static_cast<float>(h));
-      }
-      l_run[rt] = l_run[rt] * alpha + psum;
-      m_run[rt] = m_new;
-#pragma unroll
-      for (int et = 0; et < ET; ++et) {
-        o[rt][et] *= alpha;
-        o[rt][et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[et], phi, o[rt][et], 0, 0, 0);
-        o[rt][et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop[et], plo, o[rt][et], 0, 0, 0);
-      }
-    }
+  const int r0 = w * 16 + c16;
+  if (it.seg >= 0 && grp == 0 && r0 < R) {
+    const int hh = r0 / n, j = r0 - hh * n;
+    const int64_t pr = (int64_t)rq.part0 + ((int64_t)it.seg * n + j) * p.Hq + it.head_lo + hh;
+    p.part_ml[pr] = make_float2(S.m, l);
   }
-
+  __syncthreads();
+  // whole-row writes: D/4 lanes per row, 64*4/D rows per pass
+  constexpr int LPR = D / 4, RPP = 64 / LPR;
+  const int e4 = (lane % LPR) * 4;
 #pragma unroll
-  for (int rt = 0; rt < NR; ++rt) {
-    float l = l_run[rt];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    const int r = rt * 16 + c16;
+  for (int pass = 0; pass < 16 / RPP; ++pass) {
+    const int rl = pass * RPP + lane / LPR;
+    const int r = w * 16 + rl;
     if (r >= R) continue;
     const int hh = r / n, j = r - hh * n, h = it.head_lo + hh;
-    if (it.seg < 0) {
-      const float inv = 1.f / l;
-      float* op = p.out + ((int64_t)(rq.q0 + j) * p.Hq + h) * D + 4 * grp;
-#pragma unroll
-      for (int et = 0; et < ET; ++et) {
-        const f32x4 v = o[rt][et] * inv;
-        *reinterpret_cast<float4*>(op + et * 16) = make_float4(v[0], v[1], v[2], v[3]);
-      }
-    } else {
-      const int64_t pr = (int64_t)rq.part0 + ((int64_t)it.seg * n + j) * p.Hq + h;
-      float* op = p.part_o + pr * D + 4 * grp;
-#pragma unroll
-      for (int et = 0; et < ET; ++et) {
-        const f32x4 v = o[rt][et];
-        *reinterpret_cast<float4*>(op + et * 16) = make_float4(v[0], v[1], v[2], v[3]);
-      }
-      if (grp == 0) p.part_ml[pr] = make_float2(m_run[rt], l);
-    }
+    const float4 v = *reinterpret_cast<const float4*>(ost + rl * (D + 4) + e4);
+    float* dst = it.seg < 0 ? p.out + ((int64_t)(rq.q0 + j) * p.Hq + h) * D
+                            : p.part_o + ((int64_t)rq.part0 + ((int64_t)it.seg * n + j) * p.Hq + h) * D;
+    *reinterpret_cast<float4*>(dst + e4) = v;
   }
 }
 
@@ -365,12 +515,14 @@ __global__ __launch_bounds__(256) void attn_combine(AttnParams p) {
 
 template <int D>
 hipError_t launch_mfma(const AttnParams& p, int nr, hipStream_t s) {
-  dim3 grid(p.n_items), block(64);
+  constexpr int NS = 3;
+  const dim3 grid(p.n_items);
   switch (nr) {
-    case 1: attn_split_mfma<D, 1><<<grid, block, 0, s>>>(p); break;
-    case 2: attn_split_mfma<D, 2><<<grid, block, 0, s>>>(p); break;
-    case 3: attn_split_mfma<D, 3><<<grid, block, 0, s>>>(p); break;
-    case 4: attn_split_mfma<D, 4><<<grid, block, 0, s>>>(p); break;
+    case 1: attn_split_mfma<D, 1, SV_NS1><<<grid, dim3(64), 0, s>>>(p); break;
+    case 2: attn_split_mfma<D, 2, NS><<<grid, dim3(128), 0, s>>>(p); break;
+    case 3: attn_split_mfma<D, 3, NS><<<grid, dim3(192), 0, s>>>(p); break;
+    case 4: attn_split_mfma<D, 4, NS><<<grid, dim3(256), 0, s>>>(p); break;
+    case 5: attn_split_mfma<D, 5, NS><<<grid, dim3(320), 0, s>>>(p); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -378,7 +530,7 @@ hipError_t launch_mfma(const AttnParams& p, int nr, hipStream_t s) {
 
 }  // namespace
 
-int max_rows_per_item(int dtype_bf16, int D) { return dtype_bf16 ? 64 : 4096 / D; }
+int max_rows_per_item(int dtype_bf16, int D) { return dtype_bf16 ? 80 : 4096 / D; }
 
 hipError_t launch_attention(const AttnParams& p, int dtype_bf16, int nr_max, hipStream_t s) {
   hipError_t e = hipSuccess;

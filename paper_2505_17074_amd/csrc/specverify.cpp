@@ -101,12 +101,20 @@ spec_status_t check_accept(const spec_accept_args_t* a, int64_t Nq, int B) {
   return SPEC_OK;
 }
 
-// Keys per split: enough work items to fill the chip, long enough that the
-// partial outputs stay small next to the KV bytes they summarise.
-int auto_split(int64_t key_streams, int rows_max) {
-  const int64_t target_items = 2048;
-  int64_t s = (key_streams + target_items - 1) / target_items;
-  s = std::max<int64_t>(s, std::max(256, 8 * rows_max));
+// Keys per split.  With fewer (request, KV head, head group) streams than the
+// chip has compute units, streams are cut for parallelism alone (~1536
+// pieces).  Otherwise pieces aim at ~2048 items for load balance across
+// ragged lengths, but stay >= 40 * rows so the fp32 partials (rows x d x 4
+// bytes, written once and read once by the combine) remain a few percent of
+// the K/V bytes a piece streams (32 rows x d x 2 x 2 per 32 keys).
+int auto_split(int64_t key_streams, int64_t streams, int rows_max) {
+  int64_t s;
+  if (streams < 256) {
+    s = (key_streams + 1535) / 1536;
+  } else {
+    s = std::max<int64_t>((key_streams + 2047) / 2048, 40 * (int64_t)rows_max);
+  }
+  s = std::max<int64_t>(s, 256);
   s = (s + 31) / 32 * 32;
   return (int)std::min<int64_t>(s, 1 << 20);
 }
@@ -175,6 +183,11 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   }
 
   if (attn) {
+    // the bf16 kernels address one request's rows of one KV head with 32-bit offsets
+    const int64_t elem = attn->dtype == SPEC_F32 ? 4 : 2;
+    for (int i = 0; i < P.B; ++i)
+      if (((int64_t)P.reqs[i].ctx + P.reqs[i].nq) * attn->kv_stride_tok * elem >= INT32_MAX)
+        return SPEC_ERR_UNSUPPORTED;
     P.has_attn = true;
     const int bf = attn->dtype == SPEC_BF16;
     const int D = attn->head_dim;
@@ -182,7 +195,7 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
     const int rmax = sv::max_rows_per_item(bf, D);
     // query-head groups per request so that heads * n_i <= rmax
     std::vector<int> groups(P.B), hpg(P.B);
-    int64_t streams = 0;
+    int64_t streams = 0, nstreams = 0;
     int rows_max = 1;
     for (int i = 0; i < P.B; ++i) {
       const int n = P.reqs[i].nq;
@@ -191,15 +204,20 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
       hpg[i] = (G + ng - 1) / ng;                      // balanced, still <= hmax
       groups[i] = (G + hpg[i] - 1) / hpg[i];
       streams += ((int64_t)P.reqs[i].ctx + n) * Hkv * groups[i];
+      nstreams += (int64_t)Hkv * groups[i];
       rows_max = std::max(rows_max, hpg[i] * n);
     }
-    P.split = attn->split_kv > 0 ? attn->split_kv : auto_split(streams, rows_max);
+    P.split = attn->split_kv > 0 ? attn->split_kv : auto_split(streams, nstreams, rows_max);
     int64_t part = 0;
     int nr = 1;
     for (int i = 0; i < P.B; ++i) {
       ReqInfo& q = P.reqs[i];
       const int L = q.ctx + q.nq;
+      // equal 32-aligned pieces: a short trailing piece would leave its
+      // work-group idle most of the kernel while its partial costs the same
       q.nseg = (L + P.split - 1) / P.split;
+      const int piece = ((L + q.nseg - 1) / q.nseg + 31) / 32 * 32;
+      q.nseg = (L + piece - 1) / piece;
       q.part0 = (int32_t)part;
       if (q.nseg > 1) part += (int64_t)q.nseg * q.nq * Hq;
       for (int s = 0; s < q.nseg; ++s) {
@@ -210,8 +228,8 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
             it.kvh = g;
             it.head_lo = g * G + gr * hpg[i];
             it.nheads = std::min(hpg[i], G - gr * hpg[i]);
-            it.kb = s * P.split;
-            it.ke = std::min(L, (s + 1) * P.split);
+            it.kb = s * piece;
+            it.ke = std::min(L, (s + 1) * piece);
             it.seg = q.nseg > 1 ? s : -1;
             it.pad = 0;
             P.items.push_back(it);
