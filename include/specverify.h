@@ -201,8 +201,12 @@ SPEC_API spec_status_t spec_accept(const spec_requests_t* req,
                           void* host_staging, size_t host_staging_bytes,
                           void* stream);
 
-/* The whole verify step: attention then acceptance on one stream with one
- * plan upload (the logits are inputs, so the two parts are independent). */
+/* The whole verify step with one plan upload.  The logits are inputs, so the
+ * two parts are independent: the acceptance kernels run on a library-owned
+ * side stream (one per device, created on first use at the default priority)
+ * that forks from `stream` after the upload and is joined back into `stream`
+ * before the call returns, overlapping the attention kernels.  Completion is
+ * still ordered by `stream` alone. */
 SPEC_API spec_status_t spec_verify(const spec_requests_t* req,
                           const spec_attn_args_t* attn,
                           const spec_accept_args_t* acc,

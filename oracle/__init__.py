@@ -25,4 +25,4 @@ so the oracle is that definition written out, not an approximation.
 """
 from .attention import verify_attention, ancestors_or_self, widen  # noqa: F401
 from .accept import (accept_chain, accept_tree, verify_accept, softmax64,  # noqa: F401
-                     inverse_cdf, NEAR_TIE)
+                     inverse_cdf, NEAR_TIE, NEAR_TIE_MASS)

@@ -25,11 +25,16 @@ smallest BFS index on ties; accepted length = depth(n*); the final token is
 drawn from p_{n*} if n* is a leaf, else from max(0, p_{n*} - q_{n*}) (same
 zero-mass fallback).  For a path-shaped tree this is exactly the chain.
 
-Near ties.  A GPU computes p in fp32, so its decisions can legitimately
-differ from these fp64 ones only when a uniform lies within NEAR_TIE of a
-decision boundary: |u_j - min(1, p/q)| for an evaluated acceptance test, and
-the distance of the final uniform to the normalised CDF values bracketing the
-chosen token.  Every near tie on a request's decision path is reported.
+Near ties.  An implementation in finite precision can legitimately differ
+from these fp64 results only near a decision boundary, so two distances are
+reported for every request:
+  * acceptance tests on the decision path: |u_j - min(1, p/q)|, a tie below
+    NEAR_TIE = 1e-5;
+  * the final sample: the distance, in probability mass, between the target
+    u * sum(w) and the cumulative weights that bracket the chosen token, a tie
+    below NEAR_TIE_MASS = 2e-7.  (A sampler whose sums are exact to ~1e-8 of
+    probability mass -- fp64 accumulation over fp32 entries -- can only pick
+    a different token inside this band.)
 """
 from __future__ import annotations
 
@@ -40,6 +45,7 @@ import numpy as np
 from .attention import widen
 
 NEAR_TIE = 1e-5
+NEAR_TIE_MASS = 2e-7
 
 
 def softmax64(logits: np.ndarray) -> np.ndarray:
@@ -50,21 +56,21 @@ def softmax64(logits: np.ndarray) -> np.ndarray:
 
 
 def inverse_cdf(w: np.ndarray, u: float):
-    """Smallest v with cumsum(w)[v] > u * sum(w); also the normalised margin.
+    """Smallest v with cumsum(w)[v] > u * sum(w), and the distance (in the
+    units of w) from u * sum(w) to the cumulative weights bracketing v.
 
     Zero-weight tokens are never chosen; a target that rounds past the total
     is clamped to the last token with positive weight.
     """
     w = np.asarray(w, dtype=np.float64)
     cdf = np.cumsum(w)
-    total = cdf[-1]
-    v = int(np.searchsorted(cdf, u * total, side="right"))
+    target = u * cdf[-1]
+    v = int(np.searchsorted(cdf, target, side="right"))
     # cdf[v] > target >= cdf[v-1] forces w[v] > 0; only an overshoot needs a clamp
     if v >= len(w):
         v = int(np.nonzero(w > 0)[0][-1])
-    f_hi = cdf[v] / total
-    f_lo = cdf[v - 1] / total if v > 0 else 0.0
-    margin = min(abs(u - f_lo), abs(f_hi - u))
+    c_lo = cdf[v - 1] if v > 0 else 0.0
+    margin = min(abs(target - c_lo), abs(cdf[v] - target))
     return v, margin
 
 
@@ -76,6 +82,13 @@ def _test(u: float, px: float, qx: float):
     else:
         margin = np.inf
     return bool(accept), margin
+
+
+def _result(length, nxt, node, test_margins, sample_margin) -> dict:
+    mt = float(min(test_margins)) if test_margins else np.inf
+    return {"accepted_len": length, "next_token": nxt, "accepted_node": node,
+            "margin": mt, "margin_mass": float(sample_margin),
+            "near_tie": bool(mt < NEAR_TIE or sample_margin < NEAR_TIE_MASS)}
 
 
 def accept_chain(p_rows: np.ndarray, q_rows: np.ndarray, tokens: Sequence[int],
@@ -99,9 +112,7 @@ def accept_chain(p_rows: np.ndarray, q_rows: np.ndarray, tokens: Sequence[int],
     else:
         w = p_rows[k]
     nxt, m_s = inverse_cdf(w, float(uniforms[k]))
-    margins.append(m_s)
-    return {"accepted_len": a, "next_token": nxt, "accepted_node": a,
-            "margin": float(min(margins)), "near_tie": bool(min(margins) < NEAR_TIE)}
+    return _result(a, nxt, a, margins, m_s)
 
 
 def tree_depths(parent: Sequence[int]) -> np.ndarray:
@@ -140,9 +151,7 @@ def accept_tree(p_rows: np.ndarray, q_rows: dict, tokens: Sequence[int],
     else:
         w = p_rows[best]
     nxt, m_s = inverse_cdf(w, float(uniforms[n - 1]))
-    margins.append(m_s)
-    return {"accepted_len": int(depth[best]), "next_token": nxt, "accepted_node": best,
-            "margin": float(min(margins)), "near_tie": bool(min(margins) < NEAR_TIE)}
+    return _result(int(depth[best]), nxt, best, margins, m_s)
 
 
 def verify_accept(target_logits: np.ndarray, draft_probs: np.ndarray,
@@ -171,6 +180,7 @@ def verify_accept(target_logits: np.ndarray, draft_probs: np.ndarray,
     res = {key: np.full(B, -1, dtype=np.int64) for key in keys}
     res["near_tie"] = np.zeros(B, dtype=bool)
     res["margin"] = np.full(B, np.inf)
+    res["margin_mass"] = np.full(B, np.inf)
     todo = range(B) if requests is None else requests
     for i in todo:
         n = n_q[i]
@@ -187,4 +197,5 @@ def verify_accept(target_logits: np.ndarray, draft_probs: np.ndarray,
             res[key][i] = r[key]
         res["near_tie"][i] = r["near_tie"]
         res["margin"][i] = r["margin"]
+        res["margin_mass"][i] = r["margin_mass"]
     return res

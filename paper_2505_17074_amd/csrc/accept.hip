@@ -10,12 +10,14 @@
 //                      w = max(0, p - q)  (residual, node with children)
 //                      w = p              (extra token, leaf / all accepted)
 //                                                           grid B x nch
-//   acc_select       per request: prefix over chunk masses (fp64), pick the
-//                    chunk holding u * total, block scan inside it, smallest
-//                    token id whose cumulative weight exceeds the target
-//                                                           grid B
-// p = exp(l - M) / Z is computed with expf (not a fast exp2) so the fp32
-// probabilities stay within a few 1e-7 relative of the exact ones.
+//   acc_select       per request: prefix over chunk masses, pick the chunk
+//                    holding u * total, block scan inside it, smallest token
+//                    id whose cumulative weight exceeds the target   grid B
+// exp(l - max) is evaluated per entry in fp32 (expf, ~1 ulp), but every sum
+// -- the softmax normaliser Z, chunk masses, prefixes and the in-chunk scan --
+// is accumulated in fp64, and p = e / Z and the residual are formed in fp64.
+// The sampled token then follows the exact inverse CDF except where u * S
+// lies within ~1e-8 (probability mass) of a cumulative boundary.
 #include "sv_internal.h"
 
 namespace sv {
@@ -26,7 +28,7 @@ __device__ __forceinline__ float ld(const uint16_t* p, int64_t i) {
   return __uint_as_float(static_cast<uint32_t>(p[i]) << 16);
 }
 
-// Block-wide reductions over 256 threads (4 waves); `red` holds 4 floats.
+// Block-wide reductions over 256 threads (4 waves); `red` holds 4 values.
 __device__ __forceinline__ float block_max(float x, float* red) {
   for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
   __syncthreads();
@@ -34,7 +36,7 @@ __device__ __forceinline__ float block_max(float x, float* red) {
   __syncthreads();
   return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
 }
-__device__ __forceinline__ float block_sum(float x, float* red) {
+__device__ __forceinline__ double block_sum(double x, double* red) {
   for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
   __syncthreads();
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
@@ -87,7 +89,8 @@ __device__ __forceinline__ void load16_contiguous(const T* row, int base, int V,
 
 template <typename T>
 __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
-  __shared__ float red[4];
+  __shared__ float redf[4];
+  __shared__ double redd[4];
   const int row = blockIdx.x / p.nch, c = blockIdx.x % p.nch;
   const T* lp = static_cast<const T*>(p.logits) + (int64_t)row * p.l_st;
   float x[16];
@@ -95,22 +98,23 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
   float m = -INFINITY;
 #pragma unroll
   for (int k = 0; k < 16; ++k) m = fmaxf(m, x[k]);
-  m = block_max(m, red);
-  float s = 0.f;
+  m = block_max(m, redf);
+  double s = 0.0;
 #pragma unroll
-  for (int k = 0; k < 16; ++k) s += expf(x[k] - m);
-  s = block_sum(s, red);
-  if (threadIdx.x == 0) p.rowstats[(int64_t)row * p.nch + c] = make_float2(m, s);
+  for (int k = 0; k < 16; ++k) s += (double)expf(x[k] - m);
+  s = block_sum(s, redd);
+  if (threadIdx.x == 0) p.rowstats[(int64_t)row * p.nch + c] = ChunkStat{s, m, 0.f};
 }
 
 // Fold the chunk stats of one row into (M, Z) in fixed chunk order.
-__device__ __forceinline__ float2 fold_row(const AccParams& p, int row) {
-  const float2* st = p.rowstats + (int64_t)row * p.nch;
+__device__ __forceinline__ void fold_row(const AccParams& p, int row, float* M_out, double* Z_out) {
+  const ChunkStat* st = p.rowstats + (int64_t)row * p.nch;
   float M = -INFINITY;
-  for (int c = 0; c < p.nch; ++c) M = fmaxf(M, st[c].x);
-  float Z = 0.f;
-  for (int c = 0; c < p.nch; ++c) Z += st[c].y * expf(st[c].x - M);
-  return make_float2(M, Z);
+  for (int c = 0; c < p.nch; ++c) M = fmaxf(M, st[c].m);
+  double Z = 0.0;
+  for (int c = 0; c < p.nch; ++c) Z += st[c].s * exp((double)st[c].m - (double)M);
+  *M_out = M;
+  *Z_out = Z;
 }
 
 __device__ __forceinline__ int node_parent(const AccParams& p, int n) {
@@ -123,17 +127,16 @@ __device__ __forceinline__ int node_qrank(const AccParams& p, int n, int N) {
   return p.tree ? p.topo->qrank[n] : (n < N - 1 ? n : -1);
 }
 
-template <typename T>
-__device__ __forceinline__ float final_weight(float l, float q, float M, float invZ, bool residual) {
-  const float pv = expf(l - M) * invZ;
-  return residual ? fmaxf(0.f, pv - q) : pv;
+// Final-sample weight of one entry: residual max(0, p - q) or p itself.
+__device__ __forceinline__ double final_weight(float l, float q, float M, double invZ, bool residual) {
+  const double pv = (double)expf(l - M) * invZ;
+  return residual ? fmax(0.0, pv - (double)q) : pv;
 }
 
 template <typename T>
 __global__ __launch_bounds__(kAccThreads) void acc_decide_mass(AccParams p) {
-  __shared__ float red[4];
-  __shared__ int s_dec[4];
-  __shared__ float s_mz[2];
+  __shared__ double redd[4];
+  __shared__ Decision s_dec;
   const int i = blockIdx.x / p.nch, c = blockIdx.x % p.nch;
   const ReqInfo rq = p.reqs[i];
   const int N = rq.nq;
@@ -141,17 +144,20 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_mass(AccParams p) {
   const T* Q = static_cast<const T*>(p.probs);
 
   if (threadIdx.x < 64) {
+    // one lane per non-root node: the test of Eq. (1) against its parent's rows
     const int n = threadIdx.x;
     bool pass = false;
     if (n >= 1 && n < N) {
       const int par = node_parent(p, n);
       const int row = rq.q0 + par;
-      const float2 mz = fold_row(p, row);
+      float M;
+      double Z;
+      fold_row(p, row, &M, &Z);
       const int x = p.tokens[rq.q0 - i + n - 1];
-      const float px = expf(ld(L, (int64_t)row * p.l_st + x) - mz.x) / mz.y;
+      const double px = exp((double)ld(L, (int64_t)row * p.l_st + x) - (double)M) / Z;
       const int qr = rq.d0 + node_qrank(p, par, N);
-      const float qx = ld(Q, (int64_t)qr * p.p_st + x);
-      const float u = p.uniforms[rq.q0 + n - 1];
+      const double qx = (double)ld(Q, (int64_t)qr * p.p_st + x);
+      const double u = (double)p.uniforms[rq.q0 + n - 1];
       pass = u * qx < px;
     }
     const unsigned long long passmask = __ballot(pass);
@@ -166,99 +172,90 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_mass(AccParams p) {
         }
       }
       const int qrank = node_qrank(p, best, N);
-      s_dec[0] = best;
-      s_dec[1] = rq.q0 + best;
-      s_dec[2] = qrank >= 0 ? rq.d0 + qrank : -1;
-      s_dec[3] = node_depth(p, best);
-      const float2 mz = fold_row(p, rq.q0 + best);
-      s_mz[0] = mz.x;
-      s_mz[1] = mz.y;
+      Decision d;
+      d.node = best;
+      d.row = rq.q0 + best;
+      d.qrow = qrank >= 0 ? rq.d0 + qrank : -1;
+      d.len = node_depth(p, best);
+      fold_row(p, d.row, &d.M, &d.Z);
+      d.pad = 0.f;
+      s_dec = d;
     }
   }
   __syncthreads();
-  const int row = s_dec[1], qrow = s_dec[2];
-  const float M = s_mz[0], invZ = 1.f / s_mz[1];
-  const bool residual = qrow >= 0;
+  const Decision d = s_dec;
+  const double invZ = 1.0 / d.Z;
+  const bool residual = d.qrow >= 0;
   float x[16], q[16];
-  load16_coalesced(L + (int64_t)row * p.l_st, c * kAccChunk, p.V, -INFINITY, x);
-  if (residual) load16_coalesced(Q + (int64_t)qrow * p.p_st, c * kAccChunk, p.V, 0.f, q);
-  float s = 0.f;
+  load16_coalesced(L + (int64_t)d.row * p.l_st, c * kAccChunk, p.V, -INFINITY, x);
+  if (residual) load16_coalesced(Q + (int64_t)d.qrow * p.p_st, c * kAccChunk, p.V, 0.f, q);
+  double s = 0.0;
 #pragma unroll
-  for (int k = 0; k < 16; ++k) s += final_weight<T>(x[k], residual ? q[k] : 0.f, M, invZ, residual);
-  s = block_sum(s, red);
+  for (int k = 0; k < 16; ++k) s += final_weight(x[k], residual ? q[k] : 0.f, d.M, invZ, residual);
+  s = block_sum(s, redd);
   if (threadIdx.x == 0) {
     p.masses[(int64_t)i * p.nch + c] = s;
-    if (c == 0) {
-      int* d = p.decision + (int64_t)i * 8;
-      d[0] = s_dec[0];
-      d[1] = s_dec[1];
-      d[2] = s_dec[2];
-      d[3] = s_dec[3];
-      d[4] = __float_as_int(M);
-      d[5] = __float_as_int(s_mz[1]);
-    }
+    if (c == 0) p.decision[i] = d;
   }
 }
 
 template <typename T>
 __global__ __launch_bounds__(kAccThreads) void acc_select(AccParams p) {
-  __shared__ float red[4];
-  __shared__ float s_mass[kAccMaxChunks];
-  __shared__ float s_tsum[kAccThreads];
-  __shared__ double s_tot;
-  __shared__ double s_base, s_target;
+  __shared__ double redd[4];
+  __shared__ double s_mass[kAccMaxChunks];
+  __shared__ double s_tsum[kAccThreads];
+  __shared__ double s_tot, s_base, s_target;
   __shared__ int s_chunk;
   __shared__ int s_cand[4], s_last[4];
   const int i = blockIdx.x;
   const int tid = threadIdx.x;
-  const int* d = p.decision + (int64_t)i * 8;
-  const int node = d[0], row = d[1], qrow = d[2], acc_len = d[3];
-  const float M = __int_as_float(d[4]), invZ = 1.f / __int_as_float(d[5]);
-  const T* L = static_cast<const T*>(p.logits) + (int64_t)row * p.l_st;
-  const T* Q = static_cast<const T*>(p.probs) + (int64_t)(qrow >= 0 ? qrow : 0) * p.p_st;
+  const Decision d = p.decision[i];
+  const double invZ = 1.0 / d.Z;
+  const T* L = static_cast<const T*>(p.logits) + (int64_t)d.row * p.l_st;
+  const T* Q = static_cast<const T*>(p.probs) + (int64_t)(d.qrow >= 0 ? d.qrow : 0) * p.p_st;
   const float u = p.uniforms[p.reqs[i].q0 + p.reqs[i].nq - 1];
-  const float* masses = p.masses + (int64_t)i * p.nch;
+  const double* masses = p.masses + (int64_t)i * p.nch;
 
   if (tid == 0) {
     double tot = 0.0;
-    for (int c = 0; c < p.nch; ++c) tot += (double)masses[c];
+    for (int c = 0; c < p.nch; ++c) tot += masses[c];
     s_tot = tot;
   }
   __syncthreads();
   // zero residual mass (reachable only through rounding): sample from p itself
   const bool fallback = !(s_tot > 0.0);
-  const bool residual = qrow >= 0 && !fallback;
+  const bool residual = d.qrow >= 0 && !fallback;
   if (!fallback) {
     for (int c = tid; c < p.nch; c += kAccThreads) s_mass[c] = masses[c];
   } else {
     for (int c = 0; c < p.nch; ++c) {
       float x[16];
       load16_coalesced(L, c * kAccChunk, p.V, -INFINITY, x);
-      float s = 0.f;
+      double s = 0.0;
 #pragma unroll
-      for (int k = 0; k < 16; ++k) s += final_weight<T>(x[k], 0.f, M, invZ, false);
-      s = block_sum(s, red);
+      for (int k = 0; k < 16; ++k) s += final_weight(x[k], 0.f, d.M, invZ, false);
+      s = block_sum(s, redd);
       if (tid == 0) s_mass[c] = s;
     }
   }
   __syncthreads();
   if (tid == 0) {
     double tot = 0.0;
-    for (int c = 0; c < p.nch; ++c) tot += (double)s_mass[c];
+    for (int c = 0; c < p.nch; ++c) tot += s_mass[c];
     const double target = (double)u * tot;
     double cum = 0.0;
     int chosen = -1, last_pos = 0;
     for (int c = 0; c < p.nch; ++c) {
-      if (s_mass[c] > 0.f) last_pos = c;
+      if (s_mass[c] > 0.0) last_pos = c;
       if (chosen < 0) {
-        if (cum + (double)s_mass[c] > target) chosen = c;
-        else cum += (double)s_mass[c];
+        if (cum + s_mass[c] > target) chosen = c;
+        else cum += s_mass[c];
       }
     }
     if (chosen < 0) {   // target rounded past the total: last chunk with mass
       chosen = last_pos;
       cum = 0.0;
-      for (int c = 0; c < chosen; ++c) cum += (double)s_mass[c];
+      for (int c = 0; c < chosen; ++c) cum += s_mass[c];
     }
     s_chunk = chosen;
     s_base = cum;
@@ -266,28 +263,28 @@ __global__ __launch_bounds__(kAccThreads) void acc_select(AccParams p) {
   }
   __syncthreads();
   const int c = s_chunk;
-  const float tloc = (float)(s_target - s_base);
-  float x[16], q[16], w[16];
+  float x[16], q[16];
+  double w[16];
   load16_contiguous(L, c * kAccChunk, p.V, -INFINITY, x);
   if (residual) load16_contiguous(Q, c * kAccChunk, p.V, 0.f, q);
-  float tsum = 0.f;
+  double tsum = 0.0;
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
-    w[k] = final_weight<T>(x[k], residual ? q[k] : 0.f, M, invZ, residual);
+    w[k] = final_weight(x[k], residual ? q[k] : 0.f, d.M, invZ, residual);
     tsum += w[k];
   }
   // exclusive prefix of the per-thread sums, in thread (= token) order
   s_tsum[tid] = tsum;
   __syncthreads();
   if (tid < 64) {
-    const float a0 = s_tsum[4 * tid], a1 = s_tsum[4 * tid + 1], a2 = s_tsum[4 * tid + 2];
-    const float lsum = ((a0 + a1) + a2) + s_tsum[4 * tid + 3];
-    float incl = lsum;
+    const double a0 = s_tsum[4 * tid], a1 = s_tsum[4 * tid + 1], a2 = s_tsum[4 * tid + 2];
+    const double lsum = ((a0 + a1) + a2) + s_tsum[4 * tid + 3];
+    double incl = lsum;
     for (int o = 1; o < 64; o <<= 1) {
-      const float y = __shfl_up(incl, o);
+      const double y = __shfl_up(incl, o);
       if (tid >= o) incl += y;
     }
-    float ex = incl - lsum;
+    double ex = incl - lsum;
     s_tsum[4 * tid] = ex;
     ex += a0;
     s_tsum[4 * tid + 1] = ex;
@@ -297,15 +294,16 @@ __global__ __launch_bounds__(kAccThreads) void acc_select(AccParams p) {
     s_tsum[4 * tid + 3] = ex;
   }
   __syncthreads();
-  float run = s_tsum[tid];
+  double run = s_base + s_tsum[tid];
+  const double target = s_target;
   int cand = 0x7fffffff, lastpos = -1;
   const int v0 = c * kAccChunk + 16 * tid;
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
     run += w[k];
-    if (w[k] > 0.f) {
+    if (w[k] > 0.0) {
       lastpos = v0 + k;
-      if (cand == 0x7fffffff && run > tloc) cand = v0 + k;
+      if (cand == 0x7fffffff && run > target) cand = v0 + k;
     }
   }
   // smallest crossing token, else the chunk's last positive weight
@@ -322,8 +320,8 @@ __global__ __launch_bounds__(kAccThreads) void acc_select(AccParams p) {
     int best = min(min(s_cand[0], s_cand[1]), min(s_cand[2], s_cand[3]));
     if (best == 0x7fffffff) best = max(max(s_last[0], s_last[1]), max(s_last[2], s_last[3]));
     p.next_tok[i] = best;
-    p.acc_len[i] = acc_len;
-    if (p.acc_node) p.acc_node[i] = node;
+    p.acc_len[i] = d.len;
+    if (p.acc_node) p.acc_node[i] = d.node;
   }
 }
 

@@ -8,6 +8,8 @@
 // units (scores pre-multiplied by scale * log2 e) so exp2 is one v_exp_f32.
 #include "sv_internal.h"
 
+#include <algorithm>
+
 namespace sv {
 namespace {
 
@@ -528,7 +530,21 @@ hipError_t launch_mfma(const AttnParams& p, int nr, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Plan upload: the staging buffer is pinned host memory mapped into the
+// device address space, read here over the bus (an enqueued kernel, so the
+// host never waits for earlier work on the stream, unlike a small copy).
+__global__ __launch_bounds__(256) void plan_upload(const uint4* __restrict__ src, uint4* __restrict__ dst, int n16) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n16; i += gridDim.x * 256) dst[i] = src[i];
+}
+
 }  // namespace
+
+hipError_t launch_upload(const void* host_mapped, void* dst, size_t bytes, hipStream_t s) {
+  const int n16 = (int)(bytes / 16);
+  const int grid = std::min(64, std::max(1, (n16 + 255) / 256));
+  plan_upload<<<grid, 256, 0, s>>>(static_cast<const uint4*>(host_mapped), static_cast<uint4*>(dst), n16);
+  return hipGetLastError();
+}
 
 int max_rows_per_item(int dtype_bf16, int D) { return dtype_bf16 ? 80 : 4096 / D; }
 

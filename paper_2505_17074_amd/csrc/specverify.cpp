@@ -7,6 +7,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "sv_internal.h"
@@ -260,13 +261,42 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   P.off_part_ml = off;
   off = align_up(off + sizeof(float) * 2 * (size_t)P.parts);
   P.off_rowstats = off;
-  off = align_up(off + sizeof(float) * 2 * (size_t)(P.has_acc ? P.Nq * P.nch : 0));
+  off = align_up(off + sizeof(sv::ChunkStat) * (size_t)(P.has_acc ? P.Nq * P.nch : 0));
   P.off_decision = off;
-  off = align_up(off + sizeof(int32_t) * 8 * (size_t)(P.has_acc ? P.B : 0));
+  off = align_up(off + sizeof(sv::Decision) * (size_t)(P.has_acc ? P.B : 0));
   P.off_masses = off;
-  off = align_up(off + sizeof(float) * (size_t)(P.has_acc ? (int64_t)P.B * P.nch : 0));
+  off = align_up(off + sizeof(double) * (size_t)(P.has_acc ? (int64_t)P.B * P.nch : 0));
   P.device_bytes = off;
   return SPEC_OK;
+}
+
+// spec_verify runs the acceptance kernels (which read only logits, draft
+// rows, tokens and uniforms) on a side stream forked from the caller's stream
+// after the plan upload and joined back before returning, so they overlap
+// the attention kernels.  One side stream and one fork/join event pair per
+// device, created on first use at the default priority and kept for the life
+// of the process; the mutex keeps concurrent callers' fork/join pairs apart.
+struct SideStream {
+  std::mutex mu;
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  bool ready = false;
+};
+constexpr int kMaxDevices = 64;
+SideStream g_side[kMaxDevices];
+
+SideStream* side_stream() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  SideStream& S = g_side[dev];
+  std::lock_guard<std::mutex> lk(S.mu);
+  if (!S.ready) {
+    if (hipStreamCreateWithFlags(&S.s, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&S.fork, hipEventDisableTiming) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&S.join, hipEventDisableTiming) != hipSuccess) return nullptr;
+    S.ready = true;
+  }
+  return &S;
 }
 
 void write_staging(const Plan& P, void* host) {
@@ -289,14 +319,22 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* d = static_cast<char*>(ws);
   write_staging(P, staging);
-  if (hipMemcpyAsync(d, staging, P.plan_bytes, hipMemcpyHostToDevice, s) != hipSuccess) return SPEC_ERR_HIP;
+  // pinned (device-mapped) staging: a kernel pulls the plan; otherwise a copy
+  void* mapped = nullptr;
+  if (hipHostGetDevicePointer(&mapped, staging, 0) == hipSuccess && mapped &&
+      (reinterpret_cast<uintptr_t>(mapped) & 15u) == 0) {
+    if (sv::launch_upload(mapped, d, P.plan_bytes, s) != hipSuccess) return SPEC_ERR_HIP;
+  } else {
+    (void)hipGetLastError();   // clear the lookup's error state
+    if (hipMemcpyAsync(d, staging, P.plan_bytes, hipMemcpyHostToDevice, s) != hipSuccess) return SPEC_ERR_HIP;
+  }
 
   const ReqInfo* reqs = reinterpret_cast<const ReqInfo*>(d + P.off_reqs);
   const Topo* topo = reinterpret_cast<const Topo*>(d + P.off_topo);
   const int32_t* row_req = reinterpret_cast<const int32_t*>(d + P.off_rowreq);
 
+  sv::AttnParams a{};
   if (attn) {
-    sv::AttnParams a{};
     a.q = attn->q;
     a.k = attn->k;
     a.v = attn->v;
@@ -319,15 +357,9 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     a.D = attn->head_dim;
     a.n_items = (int32_t)P.items.size();
     a.Nq = (int32_t)P.Nq;
-    if (attn->event_begin && hipEventRecord(static_cast<hipEvent_t>(attn->event_begin), s) != hipSuccess)
-      return SPEC_ERR_HIP;
-    if (sv::launch_attention(a, attn->dtype == SPEC_BF16, P.nr_max, s) != hipSuccess) return SPEC_ERR_HIP;
-    if (attn->event_end && hipEventRecord(static_cast<hipEvent_t>(attn->event_end), s) != hipSuccess)
-      return SPEC_ERR_HIP;
-    if (P.parts > 0 && sv::launch_combine(a, s) != hipSuccess) return SPEC_ERR_HIP;
   }
+  sv::AccParams c{};
   if (acc) {
-    sv::AccParams c{};
     c.logits = acc->target_logits;
     c.probs = acc->draft_probs ? acc->draft_probs : acc->target_logits;
     c.l_st = acc->logits_stride;
@@ -340,21 +372,47 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     c.reqs = reqs;
     c.topo = topo;
     c.row_req = row_req;
-    c.rowstats = reinterpret_cast<float2*>(d + P.off_rowstats);
-    c.decision = reinterpret_cast<int32_t*>(d + P.off_decision);
-    c.masses = reinterpret_cast<float*>(d + P.off_masses);
+    c.rowstats = reinterpret_cast<sv::ChunkStat*>(d + P.off_rowstats);
+    c.decision = reinterpret_cast<sv::Decision*>(d + P.off_decision);
+    c.masses = reinterpret_cast<double*>(d + P.off_masses);
     c.V = acc->vocab;
     c.nch = P.nch;
     c.B = P.B;
     c.Nq = (int32_t)P.Nq;
     c.tree = P.tree ? 1 : 0;
     c.bf16 = acc->dtype == SPEC_BF16;
-    if (acc->event_begin && hipEventRecord(static_cast<hipEvent_t>(acc->event_begin), s) != hipSuccess)
-      return SPEC_ERR_HIP;
-    if (sv::launch_accept(c, s) != hipSuccess) return SPEC_ERR_HIP;
-    if (acc->event_end && hipEventRecord(static_cast<hipEvent_t>(acc->event_end), s) != hipSuccess)
-      return SPEC_ERR_HIP;
   }
+
+  auto launch_acc = [&](hipStream_t st) -> bool {
+    if (acc->event_begin && hipEventRecord(static_cast<hipEvent_t>(acc->event_begin), st) != hipSuccess) return false;
+    if (sv::launch_accept(c, st) != hipSuccess) return false;
+    if (acc->event_end && hipEventRecord(static_cast<hipEvent_t>(acc->event_end), st) != hipSuccess) return false;
+    return true;
+  };
+  auto launch_attn = [&](hipStream_t st) -> bool {
+    if (attn->event_begin && hipEventRecord(static_cast<hipEvent_t>(attn->event_begin), st) != hipSuccess)
+      return false;
+    if (sv::launch_attention(a, attn->dtype == SPEC_BF16, P.nr_max, st) != hipSuccess) return false;
+    if (attn->event_end && hipEventRecord(static_cast<hipEvent_t>(attn->event_end), st) != hipSuccess) return false;
+    if (P.parts > 0 && sv::launch_combine(a, st) != hipSuccess) return false;
+    return true;
+  };
+
+  if (attn && acc) {
+    SideStream* S = side_stream();
+    if (!S) return SPEC_ERR_HIP;
+    std::lock_guard<std::mutex> lk(S->mu);
+    if (hipEventRecord(S->fork, s) != hipSuccess || hipStreamWaitEvent(S->s, S->fork, 0) != hipSuccess)
+      return SPEC_ERR_HIP;
+    if (!launch_acc(S->s)) return SPEC_ERR_HIP;
+    if (hipEventRecord(S->join, S->s) != hipSuccess) return SPEC_ERR_HIP;
+    const bool ok = launch_attn(s);
+    // join even after a failed launch, so the caller's stream never runs ahead
+    if (hipStreamWaitEvent(s, S->join, 0) != hipSuccess || !ok) return SPEC_ERR_HIP;
+    return SPEC_OK;
+  }
+  if (attn && !launch_attn(s)) return SPEC_ERR_HIP;
+  if (acc && !launch_acc(s)) return SPEC_ERR_HIP;
   return SPEC_OK;
 }
 

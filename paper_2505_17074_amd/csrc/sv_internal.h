@@ -61,6 +61,22 @@ struct AttnParams {
   int32_t Nq;
 };
 
+// Acceptance scratch: per (row, vocabulary chunk) max and fp64 sum of exp.
+struct ChunkStat {
+  double s;
+  float m;
+  float pad;
+};
+
+// Per request: the accepted node, the row the final token is drawn from, its
+// draft row (-1: the extra token is drawn from p itself) and normaliser.
+struct Decision {
+  int32_t node, row, qrow, len;
+  float M;      // row max
+  float pad;
+  double Z;     // sum of exp(l - M), fp64
+};
+
 struct AccParams {
   const void* logits;
   const void* probs;
@@ -73,9 +89,9 @@ struct AccParams {
   const ReqInfo* reqs;
   const Topo* topo;
   const int32_t* row_req;
-  float2* rowstats;    // [Nq, nch] (chunk max, chunk sum of exp)
-  int32_t* decision;   // [B, 8]: accepted node, sample row, draft row or -1, accepted len, M, Z bits
-  float* masses;       // [B, nch]
+  ChunkStat* rowstats;   // [Nq, nch]
+  Decision* decision;    // [B]
+  double* masses;        // [B, nch] final-sample weight mass per chunk
   int32_t V, nch, B, Nq;
   int32_t tree;        // 1 = tree mode
   int32_t bf16;
@@ -89,5 +105,6 @@ int max_rows_per_item(int dtype_bf16, int D);
 hipError_t launch_attention(const AttnParams& p, int dtype_bf16, int nr_max, hipStream_t s);
 hipError_t launch_combine(const AttnParams& p, hipStream_t s);
 hipError_t launch_accept(const AccParams& p, hipStream_t s);
+hipError_t launch_upload(const void* host_mapped, void* dst, size_t bytes, hipStream_t s);
 
 }  // namespace sv
