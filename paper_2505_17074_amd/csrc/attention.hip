@@ -15,6 +15,9 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
@@ -59,8 +62,23 @@ __device__ __forceinline__ bool visible(int t, int ctx, uint32_t anc) {
 // 16e + i.  The item's output is staged through LDS and written as rows.
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void lds_void_t;
-#ifndef SV_NS1
-#define SV_NS1 3
+// Ring depth (tiles in LDS) by waves per work-group.  Fewer work-groups fit on
+// a compute unit as W grows (registers), so deeper rings keep enough bytes in
+// flight per compute unit.
+#ifndef SV_NS_W1
+#define SV_NS_W1 3
+#endif
+#ifndef SV_NS_W2
+#define SV_NS_W2 3
+#endif
+#ifndef SV_NS_W3
+#define SV_NS_W3 3
+#endif
+#ifndef SV_NS_W4
+#define SV_NS_W4 3
+#endif
+#ifndef SV_NS_W5
+#define SV_NS_W5 3
 #endif
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4_t;
@@ -94,6 +112,16 @@ template <int N>
 __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Work-group barrier for the tile ring.  __syncthreads() is a release fence at
+// work-group scope, which the compiler implements for a kernel with LDS-bound
+// transfers by waiting for all of them (vmcnt(0)), draining the ring.  Here the
+// caller has already waited for the transfers the next tile needs; the barrier
+// only has to order LDS accesses, and the memory clobber keeps the compiler
+// from moving loads or stores across it.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 template <int D, int W>
@@ -189,59 +217,82 @@ __device__ __forceinline__ void compute_tile(const char* stage, RowTile<D>& S, i
   // the accumulators to the matrix cores alone.
   constexpr float kLazy = 8.f;
   float sv[8];
-  bool need = false;
   if (t0 + 32 <= min(ke, ctx)) {      // wave-uniform: every key visible to every row
 #pragma unroll
-    for (int x = 0; x < 8; ++x) {
-      sv[x] = s[x >> 2][x & 3] * scale_log2;
-      need |= sv[x] > S.m + kLazy;
-    }
+    for (int x = 0; x < 8; ++x) sv[x] = s[x >> 2][x & 3] * scale_log2;
   } else {
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int t = t0 + 8 * grp + 4 * kt + i;
-        float x = s[kt][i] * scale_log2;
-        if (t >= ke || !visible(t, ctx, S.anc)) x = -INFINITY;
-        sv[kt * 4 + i] = x;
-        need |= x > S.m + kLazy;
+        const float x = s[kt][i] * scale_log2;
+        sv[kt * 4 + i] = (t >= ke || !visible(t, ctx, S.anc)) ? -INFINITY : x;
       }
     }
   }
-  if (__any(need)) {                  // wave-uniform
-    float mloc = sv[0];
-#pragma unroll
-    for (int x = 1; x < 8; ++x) mloc = fmaxf(mloc, sv[x]);
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+  // this lane's largest score (a masked -inf never wins over a finite one)
+  const float mloc0 = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
+                            fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+  if (__any(mloc0 > S.m + kLazy)) {   // wave-uniform
+    float mloc = fmaxf(mloc0, __shfl_xor(mloc0, 16));
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
     const float m_new = fmaxf(S.m, mloc);
-    const float alpha = (m_new == S.m) ? 1.f : exp2f(S.m - m_new);    // S.m = -inf gives 0
+    // exp2 of a non-positive argument; S.m = -inf gives 0
+    const float alpha = (m_new == S.m) ? 1.f : __builtin_amdgcn_exp2f(S.m - m_new);
     S.l *= alpha;
 #pragma unroll
     for (int et = 0; et < ET; ++et) S.o[et] *= alpha;
     S.m = m_new;
   }
   const float m_use = (S.m == -INFINITY) ? 0.f : S.m;
+  // p = 2^(score - m) <= 2^kLazy with the hardware exp2 (arguments are at most
+  // kLazy; results below the normal range flush to zero, negligible against l >= 1
+  // once a row has a finite score).  p is split into bf16 hi + lo so the PV
+  // products keep about 16 significant bits of p.
+  float pv[8];
   float psum = 0.f;
-  bf16x8 phi, plo;
 #pragma unroll
   for (int x = 0; x < 8; ++x) {
-    const float pv = exp2f(sv[x] - m_use);
-    psum += pv;
-    const __bf16 h = static_cast<__bf16>(pv);
-    phi[x] = h;
-    plo[x] = static_cast<__bf16>(pv - static_cast<float>(h));
+    pv[x] = __builtin_amdgcn_exp2f(sv[x] - m_use);
+    psum += pv[x];
   }
   S.l += psum;
-  const char* vbase = stage + G::MAT;
+  uint32_t hw[4], lw[4];
 #pragma unroll
-  for (int et = 0; et < ET; ++et) {
-    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vbase + S.voff[et]));
-    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(vbase + S.voff[et] + 4 * G::ROWB));
-    const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-    S.o[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, phi, S.o[et], 0, 0, 0);
-    S.o[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, plo, S.o[et], 0, 0, 0);
+  for (int i = 0; i < 4; ++i) {
+    const bf16x2 h2 = __builtin_convertvector((f32x2){pv[2 * i], pv[2 * i + 1]}, bf16x2);
+    hw[i] = __builtin_bit_cast(uint32_t, h2);
+    const float h0 = __uint_as_float(hw[i] << 16), h1 = __uint_as_float(hw[i] & 0xffff0000u);
+    lw[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){pv[2 * i] - h0, pv[2 * i + 1] - h1}, bf16x2));
+  }
+  const bf16x8 phi = __builtin_bit_cast(bf16x8, (u32x4){hw[0], hw[1], hw[2], hw[3]});
+  const bf16x8 plo = __builtin_bit_cast(bf16x8, (u32x4){lw[0], lw[1], lw[2], lw[3]});
+  // V^T operands by transposing LDS reads, in groups of VG column tiles.  The
+  // reads are issued from inline assembly with their own lgkmcnt waits: the
+  // compiler's builtin for this read makes it wait for every outstanding
+  // LDS-bound transfer (vmcnt(0)), which would serialise the ring.
+  const uint32_t vbase = (uint32_t)(uintptr_t)(stage + G::MAT);
+  constexpr int VG = 4;
+#pragma unroll
+  for (int e0 = 0; e0 < ET; e0 += VG) {
+    s16x4 lo[VG], hi[VG];
+#pragma unroll
+    for (int e = 0; e < VG; ++e) {
+      const uint32_t a = vbase + (uint32_t)S.voff[e0 + e];
+      asm volatile("ds_read_b64_tr_b16 %0, %2\n\tds_read_b64_tr_b16 %1, %2 offset:%3"
+                   : "=v"(lo[e]), "=v"(hi[e])
+                   : "v"(a), "i"(4 * G::ROWB));
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(lo[0]), "+v"(hi[0]), "+v"(lo[1]), "+v"(hi[1]), "+v"(lo[2]), "+v"(hi[2]), "+v"(lo[3]),
+                   "+v"(hi[3]));
+#pragma unroll
+    for (int e = 0; e < VG; ++e) {
+      const bf16x8 vop = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo[e], hi[e], 0, 1, 2, 3, 4, 5, 6, 7));
+      S.o[e0 + e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, phi, S.o[e0 + e], 0, 0, 0);
+      S.o[e0 + e] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, plo, S.o[e0 + e], 0, 0, 0);
+    }
   }
 }
 
@@ -249,7 +300,13 @@ template <int D, int W, int NS>
 struct AttnLds {
   static constexpr int RING = NS * Geo<D>::STAGE;
   static constexpr int OUT = W * 16 * (D + 4) * 4;  // fp32 output staging, padded rows
-  static constexpr int BYTES = RING > OUT ? RING : OUT;
+  static constexpr int MAIN = RING > OUT ? RING : OUT;
+  // The query rows (16 bf16 rows per wave) sit in the ring's last stage, which
+  // the first tile transfer into it only overwrites after the first barrier.
+  static constexpr int QT = 16 * Geo<D>::ROWB;
+  static constexpr int QOFF = (NS - 1) * Geo<D>::STAGE;
+  static constexpr int QEND = QOFF + W * QT;
+  static constexpr int BYTES = MAIN > QEND ? MAIN : QEND;
 };
 
 template <int D, int W, int NS>
@@ -264,18 +321,32 @@ __global__ __launch_bounds__(64 * W) void attn_split_mfma(AttnParams p) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c16 = lane & 15, grp = lane >> 4;
   const AttnItem it = p.items[blockIdx.x];
-  const ReqInfo rq = p.reqs[it.req];
-  const int n = rq.nq;
+  const int n = it.nq;
   const int R = it.nheads * n;
-  const int ctx = rq.ctx;
+  const int ctx = it.ctx;
   const int row_bytes = (int)(p.kv_st * 2);
-  const char* Kb = static_cast<const char*>(p.k) + ((int64_t)rq.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh) * 2;
-  const char* Vb = static_cast<const char*>(p.v) + ((int64_t)rq.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh) * 2;
+  const char* Kb = static_cast<const char*>(p.k) + ((int64_t)it.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh) * 2;
+  const char* Vb = static_cast<const char*>(p.v) + ((int64_t)it.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh) * 2;
   const int ntiles = (it.ke - it.kb + 31) / 32;
   // byte range of this request's rows for this KV head (the host keeps it < 2^31)
-  const int range = (rq.ctx + rq.nq) * row_bytes;
+  const int range = (it.ctx + it.nq) * row_bytes;
   const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)Kb, 0, range, 0x00020000);
   const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)Vb, 0, range, 0x00020000);
+  char* qlds = lds + AttnLds<D, W, NS>::QOFF + w * AttnLds<D, W, NS>::QT;
+
+  // This wave's 16 query rows go HBM -> LDS with the same direct transfers as
+  // K/V (no register loads are pending when the tile loop starts, so nothing
+  // waits on more than the oldest tile).  Padding rows repeat the item's row 0.
+#pragma unroll
+  for (int jj = 0; jj < 16 / G::RPI; ++jj) {
+    const int rl = jj * G::RPI + lane / G::CH;
+    int rr = w * 16 + rl;
+    if (rr >= R) rr = 0;
+    const int hh = rr / n, j = rr - hh * n;
+    const char* src = static_cast<const char*>(p.q) +
+                      ((int64_t)(it.q0 + j) * p.q_st + (int64_t)(it.head_lo + hh) * p.q_sh) * 2 + (lane % G::CH) * 16;
+    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(qlds + jj * 1024), 16, 0, 0);
+  }
 
   XferPlan<D, W> X;
 #pragma unroll
@@ -287,46 +358,58 @@ __global__ __launch_bounds__(64 * W) void attn_split_mfma(AttnParams p) {
   RowTile<D> S;
   {
     const int r = w * 16 + c16;
-    if (r < R) {
-      const int hh = r / n, j = r - hh * n;
-      const uint16_t* qp = static_cast<const uint16_t*>(p.q) + (int64_t)(rq.q0 + j) * p.q_st +
-                           (int64_t)(it.head_lo + hh) * p.q_sh + grp * 8;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) S.q[ks] = *reinterpret_cast<const bf16x8*>(qp + ks * 32);
-      S.anc = p.topo->anc[j];
-    } else {
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) S.q[ks] = bf16x8{};
-      S.anc = 0u;
+    const int j = (r < R) ? r % n : -1;
+    // A uniform loop over the kernel-argument table: each entry is pinned to a
+    // scalar register so the selection cannot become a per-lane vector load.
+    uint32_t anc = 0u;
+    for (int jj = 0; jj < n; ++jj) {
+      uint32_t a = p.anc[jj];
+      asm volatile("" : "+s"(a));
+      anc = (j == jj) ? a : anc;
     }
+    S.anc = anc;
     S.m = -INFINITY;
     S.l = 0.f;
 #pragma unroll
     for (int et = 0; et < ET; ++et) S.o[et] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int rk = 8 * (c16 >> 2) + (c16 & 3);
+    const int rk0 = 8 * (c16 >> 2) + (c16 & 3);
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) S.koff[ks] = rk * G::ROWB + (((ks * 4 + grp) ^ swk<D>(rk)) * 16);
-    const int rv = 8 * grp + (c16 >> 2);
+    for (int ks = 0; ks < KS; ++ks) S.koff[ks] = rk0 * G::ROWB + (((ks * 4 + grp) ^ swk<D>(rk0)) * 16);
+    const int rv0 = 8 * grp + (c16 >> 2);
 #pragma unroll
     for (int et = 0; et < ET; ++et)
-      S.voff[et] = rv * G::ROWB + (((2 * et + ((c16 & 3) >> 1)) ^ swv<D>(rv)) * 16) + (c16 & 1) * 8;
+      S.voff[et] = rv0 * G::ROWB + (((2 * et + ((c16 & 3) >> 1)) ^ swv<D>(rv0)) * 16) + (c16 & 1) * 8;
   }
   const bool active = w * 16 < R;     // wave-uniform: this wave has query rows
 
-  // the ring's first NS-1 tiles go out after the query loads
+  // the ring's first NS-1 tiles (only tiles of the item are ever transferred)
 #pragma unroll
   for (int st = 0; st < NS - 1; ++st)
-    issue_tile<D, W>(lds + st * G::STAGE, rk, rv, row_bytes, it.kb + 32 * st, it.ke, w, lane, X);
+    if (st < ntiles) issue_tile<D, W>(lds + st * G::STAGE, rk, rv, row_bytes, it.kb + 32 * st, it.ke, w, lane, X);
 
+  // The query rows are this wave's oldest transfers, so they have landed once
+  // the first tile's wait passes; they are read before the first barrier, after
+  // which stage NS-1 is refilled.
+  bool have_q = false;
   for (int tb = 0; tb < ntiles; tb += NS) {
 #pragma unroll
     for (int st = 0; st < NS; ++st) {           // stage index is a compile-time constant
       const int t = tb + st;
       if (t >= ntiles) break;
-      wait_vm<PER * (NS - 2)>();      // this wave's transfers of tile t have landed
-      __syncthreads();                // ... and everyone's; stage (t-1) % NS is free
-      issue_tile<D, W>(lds + ((st + NS - 1) % NS) * G::STAGE, rk, rv, row_bytes, it.kb + 32 * (t + NS - 1), it.ke,
-                       w, lane, X);
+      // this wave's transfers of tile t have landed: NS-2 later tiles may still
+      // be in flight, none in the item's last NS-2 tiles (over-waiting there)
+      if (t + NS - 2 < ntiles) wait_vm<PER * (NS - 2)>();
+      else wait_vm<0>();
+      if (!have_q) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          S.q[ks] = *reinterpret_cast<const bf16x8*>(qlds + c16 * G::ROWB + (ks * 4 + grp) * 16);
+        have_q = true;
+      }
+      ring_barrier();                 // everyone's have landed; stage (t-1) % NS is free
+      if (t + NS - 1 < ntiles)
+        issue_tile<D, W>(lds + ((st + NS - 1) % NS) * G::STAGE, rk, rv, row_bytes, it.kb + 32 * (t + NS - 1), it.ke,
+                         w, lane, X);
       if (active) compute_tile<D>(lds + st * G::STAGE, S, it.kb + 32 * t, it.ke, ctx, p.scale_log2, lane);
     }
   }
@@ -347,7 +430,7 @@ __global__ __launch_bounds__(64 * W) void attn_split_mfma(AttnParams p) {
   const int r0 = w * 16 + c16;
   if (it.seg >= 0 && grp == 0 && r0 < R) {
     const int hh = r0 / n, j = r0 - hh * n;
-    const int64_t pr = (int64_t)rq.part0 + ((int64_t)it.seg * n + j) * p.Hq + it.head_lo + hh;
+    const int64_t pr = (int64_t)it.part0 + ((int64_t)it.seg * n + j) * p.Hq + it.head_lo + hh;
     p.part_ml[pr] = make_float2(S.m, l);
   }
   __syncthreads();
@@ -361,8 +444,8 @@ __global__ __launch_bounds__(64 * W) void attn_split_mfma(AttnParams p) {
     if (r >= R) continue;
     const int hh = r / n, j = r - hh * n, h = it.head_lo + hh;
     const float4 v = *reinterpret_cast<const float4*>(ost + rl * (D + 4) + e4);
-    float* dst = it.seg < 0 ? p.out + ((int64_t)(rq.q0 + j) * p.Hq + h) * D
-                            : p.part_o + ((int64_t)rq.part0 + ((int64_t)it.seg * n + j) * p.Hq + h) * D;
+    float* dst = it.seg < 0 ? p.out + ((int64_t)(it.q0 + j) * p.Hq + h) * D
+                            : p.part_o + ((int64_t)it.part0 + ((int64_t)it.seg * n + j) * p.Hq + h) * D;
     *reinterpret_cast<float4*>(dst + e4) = v;
   }
 }
@@ -517,14 +600,13 @@ __global__ __launch_bounds__(256) void attn_combine(AttnParams p) {
 
 template <int D>
 hipError_t launch_mfma(const AttnParams& p, int nr, hipStream_t s) {
-  constexpr int NS = 3;
   const dim3 grid(p.n_items);
   switch (nr) {
-    case 1: attn_split_mfma<D, 1, SV_NS1><<<grid, dim3(64), 0, s>>>(p); break;
-    case 2: attn_split_mfma<D, 2, NS><<<grid, dim3(128), 0, s>>>(p); break;
-    case 3: attn_split_mfma<D, 3, NS><<<grid, dim3(192), 0, s>>>(p); break;
-    case 4: attn_split_mfma<D, 4, NS><<<grid, dim3(256), 0, s>>>(p); break;
-    case 5: attn_split_mfma<D, 5, NS><<<grid, dim3(320), 0, s>>>(p); break;
+    case 1: attn_split_mfma<D, 1, SV_NS_W1><<<grid, dim3(64), 0, s>>>(p); break;
+    case 2: attn_split_mfma<D, 2, SV_NS_W2><<<grid, dim3(128), 0, s>>>(p); break;
+    case 3: attn_split_mfma<D, 3, SV_NS_W3><<<grid, dim3(192), 0, s>>>(p); break;
+    case 4: attn_split_mfma<D, 4, SV_NS_W4><<<grid, dim3(256), 0, s>>>(p); break;
+    case 5: attn_split_mfma<D, 5, SV_NS_W5><<<grid, dim3(320), 0, s>>>(p); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -232,13 +232,24 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
             it.kb = s * piece;
             it.ke = std::min(L, (s + 1) * piece);
             it.seg = q.nseg > 1 ? s : -1;
-            it.pad = 0;
+            it.ctx = q.ctx;
+            it.nq = q.nq;
+            it.q0 = q.q0;
+            it.kv0 = q.kv0;
+            it.part0 = q.part0;
+            it.pad[0] = it.pad[1] = it.pad[2] = it.pad[3] = 0;
             P.items.push_back(it);
             nr = std::max(nr, (it.nheads * q.nq + 15) / 16);
           }
         }
       }
     }
+    // Longest items first: work-groups are dispatched in index order as slots
+    // free up, so the last ones to start are the shortest and the kernel's
+    // tail (slots idling while a few long items finish) stays short.
+    std::stable_sort(P.items.begin(), P.items.end(), [](const AttnItem& x, const AttnItem& y) {
+      return (x.ke - x.kb + 31) / 32 > (y.ke - y.kb + 31) / 32;
+    });
     if (part >= INT32_MAX) return SPEC_ERR_INVALID_ARG;
     P.parts = part;
     P.nr_max = nr;
@@ -357,6 +368,7 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     a.D = attn->head_dim;
     a.n_items = (int32_t)P.items.size();
     a.Nq = (int32_t)P.Nq;
+    std::memcpy(a.anc, P.topo.anc, sizeof(a.anc));
   }
   sv::AccParams c{};
   if (acc) {

@@ -23,6 +23,8 @@ struct ReqInfo {
 };
 
 // One attention work item: a KV range of one (request, KV head, query-head group).
+// The request's fields are repeated here so a work-group needs one scalar
+// load of 64 bytes before it can issue its first transfer.
 struct AttnItem {
   int32_t req;
   int32_t kvh;
@@ -30,7 +32,12 @@ struct AttnItem {
   int32_t nheads;   // query heads in the group (rows = nheads * n_i)
   int32_t kb, ke;   // KV positions [kb, ke) relative to the request's first KV row
   int32_t seg;      // split index (partial slot) or -1 for direct output
-  int32_t pad;
+  int32_t ctx;      // the request's c_i, n_i, first query row, first KV row, first partial
+  int32_t nq;
+  int32_t q0;
+  int32_t kv0;
+  int32_t part0;
+  int32_t pad[4];
 };
 
 // Tree / chain topology tables (one per step).
@@ -59,6 +66,7 @@ struct AttnParams {
   int32_t Hq, Hkv, G, D;
   int32_t n_items;
   int32_t Nq;
+  uint32_t anc[kMaxNodes];   // ancestors-or-self masks (kernel arguments: uniform loads)
 };
 
 // Acceptance scratch: per (row, vocabulary chunk) max and fp64 sum of exp.
