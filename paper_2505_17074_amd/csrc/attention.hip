@@ -281,7 +281,7 @@ __device__ __forceinline__ void compute_tile(const char* stage, RowTile<D>& S, i
     for (int e = 0; e < VG; ++e) {
       const uint32_t a = vbase + (uint32_t)S.voff[e0 + e];
       asm volatile("ds_read_b64_tr_b16 %0, %2\n\tds_read_b64_tr_b16 %1, %2 offset:%3"
-                   : "=v"(lo[e]), "=v"(hi[e])
+                   : "=&v"(lo[e]), "=&v"(hi[e])   // early clobber: the address is read twice
                    : "v"(a), "i"(4 * G::ROWB));
     }
     asm volatile("s_waitcnt lgkmcnt(0)"
@@ -362,7 +362,7 @@ __global__ __launch_bounds__(64 * W) void attn_split_mfma(AttnParams p) {
     // A uniform loop over the kernel-argument table: each entry is pinned to a
     // scalar register so the selection cannot become a per-lane vector load.
     uint32_t anc = 0u;
-    for (int jj = 0; jj < n; ++jj) {
+    for (int jj = 0; jj < min(n, kMaxNodes); ++jj) {
       uint32_t a = p.anc[jj];
       asm volatile("" : "+s"(a));
       anc = (j == jj) ? a : anc;
@@ -427,12 +427,16 @@ __global__ __launch_bounds__(64 * W) void attn_split_mfma(AttnParams p) {
     const f32x4 v = S.o[et] * scale;
     *reinterpret_cast<float4*>(ost + c16 * (D + 4) + et * 16 + 4 * grp) = make_float4(v[0], v[1], v[2], v[3]);
   }
-  const int r0 = w * 16 + c16;
-  if (it.seg >= 0 && grp == 0 && r0 < R) {
-    const int hh = r0 / n, j = r0 - hh * n;
-    const int64_t pr = (int64_t)it.part0 + ((int64_t)it.seg * n + j) * p.Hq + it.head_lo + hh;
-    p.part_ml[pr] = make_float2(S.m, l);
-  }
+  // output row of query row r (rows outside the destination are never written)
+  auto out_row = [&](int r) -> int64_t {
+    const int hh = r / n, j = r - hh * n, h = it.head_lo + hh;
+    const int64_t o = it.seg < 0 ? (int64_t)(it.q0 + j) * p.Hq + h
+                                 : (int64_t)it.part0 + ((int64_t)it.seg * n + j) * p.Hq + h;
+    const int64_t lim = it.seg < 0 ? (int64_t)p.Nq * p.Hq : (int64_t)p.n_parts;
+    return (r < R && o >= 0 && o < lim) ? o : -1;
+  };
+  const int64_t o0 = out_row(w * 16 + c16);
+  if (it.seg >= 0 && grp == 0 && o0 >= 0) p.part_ml[o0] = make_float2(S.m, l);
   __syncthreads();
   // whole-row writes: D/4 lanes per row, 64*4/D rows per pass
   constexpr int LPR = D / 4, RPP = 64 / LPR;
@@ -440,13 +444,10 @@ __global__ __launch_bounds__(64 * W) void attn_split_mfma(AttnParams p) {
 #pragma unroll
   for (int pass = 0; pass < 16 / RPP; ++pass) {
     const int rl = pass * RPP + lane / LPR;
-    const int r = w * 16 + rl;
-    if (r >= R) continue;
-    const int hh = r / n, j = r - hh * n, h = it.head_lo + hh;
+    const int64_t o = out_row(w * 16 + rl);
+    if (o < 0) continue;
     const float4 v = *reinterpret_cast<const float4*>(ost + rl * (D + 4) + e4);
-    float* dst = it.seg < 0 ? p.out + ((int64_t)(it.q0 + j) * p.Hq + h) * D
-                            : p.part_o + ((int64_t)it.part0 + ((int64_t)it.seg * n + j) * p.Hq + h) * D;
-    *reinterpret_cast<float4*>(dst + e4) = v;
+    *reinterpret_cast<float4*>((it.seg < 0 ? p.out : p.part_o) + o * D + e4) = v;
   }
 }
 

@@ -360,6 +360,7 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     a.reqs = reqs;
     a.topo = topo;
     a.row_req = row_req;
+    a.n_parts = (int32_t)P.parts;
     const float scale = attn->scale > 0.f ? attn->scale : 1.f / std::sqrt((float)attn->head_dim);
     a.scale_log2 = scale * 1.4426950408889634f;
     a.Hq = attn->num_q_heads;

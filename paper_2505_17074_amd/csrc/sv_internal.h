@@ -62,6 +62,7 @@ struct AttnParams {
   const ReqInfo* reqs;
   const Topo* topo;
   const int32_t* row_req;   // query row -> request
+  int32_t n_parts;           // rows of the partial buffers
   float scale_log2;   // scale * log2(e)
   int32_t Hq, Hkv, G, D;
   int32_t n_items;
