@@ -1,18 +1,19 @@
 // Speculative acceptance and final sample for gfx950.
 //
-// Three launches, each streaming what it needs once:
-//   acc_rowstats     every target-logit row in 4096-entry chunks: chunk max
-//                    and chunk sum of exp(l - max)          grid Nq x nch
-//   acc_decide_mass  per (request, chunk): fold the chunk stats of the rows
-//                    the tests need, run the acceptance tests (one lane per
-//                    draft node), walk to the deepest accepted node, then
-//                    the chunk's mass of the final-sample weights
-//                      w = max(0, p - q)  (residual, node with children)
-//                      w = p              (extra token, leaf / all accepted)
-//                                                           grid B x nch
-//   acc_select       per request: prefix over chunk masses, pick the chunk
-//                    holding u * total, block scan inside it, smallest token
-//                    id whose cumulative weight exceeds the target   grid B
+// Two launches, each streaming what it needs once:
+//   acc_rowstats       every target-logit row in 4096-entry chunks: chunk max
+//                      and chunk sum of exp(l - max)          grid Nq x nch
+//   acc_decide_select  per (request, chunk): fold the chunk stats of the
+//                      request's rows, run the acceptance tests (one lane per
+//                      draft node), walk to the deepest accepted node, then
+//                      the chunk's mass of the final-sample weights
+//                        w = max(0, p - q)  (residual, node with children)
+//                        w = p              (extra token, leaf / all accepted)
+//                      the request's last work-group to publish its mass then
+//                      takes the prefix over chunk masses, picks the chunk
+//                      holding u * total, scans inside it and emits the
+//                      smallest token id whose cumulative weight exceeds the
+//                      target                                grid B x nch
 // exp(l - max) is evaluated per entry in fp32 (expf, ~1 ulp), but every sum
 // -- the softmax normaliser Z, chunk masses, prefixes and the in-chunk scan --
 // is accumulated in fp64, and p = e / Z and the residual are formed in fp64.
@@ -106,17 +107,6 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
   if (threadIdx.x == 0) p.rowstats[(int64_t)row * p.nch + c] = ChunkStat{s, m, 0.f};
 }
 
-// Fold the chunk stats of one row into (M, Z) in fixed chunk order.
-__device__ __forceinline__ void fold_row(const AccParams& p, int row, float* M_out, double* Z_out) {
-  const ChunkStat* st = p.rowstats + (int64_t)row * p.nch;
-  float M = -INFINITY;
-  for (int c = 0; c < p.nch; ++c) M = fmaxf(M, st[c].m);
-  double Z = 0.0;
-  for (int c = 0; c < p.nch; ++c) Z += st[c].s * exp((double)st[c].m - (double)M);
-  *M_out = M;
-  *Z_out = Z;
-}
-
 __device__ __forceinline__ int node_parent(const AccParams& p, int n) {
   return p.tree ? p.topo->parent[n] : n - 1;
 }
@@ -133,32 +123,84 @@ __device__ __forceinline__ double final_weight(float l, float q, float M, double
   return residual ? fmax(0.0, pv - (double)q) : pv;
 }
 
+// Device-scope (all XCDs) publication of the chunk masses between the
+// work-groups of one request: the stores write through to the device
+// coherence point, the loads read from it, and the ticket is a device-scope
+// atomic issued after this wave's stores have completed.  No cache-wide
+// write-back is needed since nothing else is handed over.
+__device__ __forceinline__ void store_dev(double* p, double v) {
+  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), __double_as_longlong(v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double load_dev(const double* p) {
+  return __longlong_as_double(__hip_atomic_load(reinterpret_cast<const unsigned long long*>(p), __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT));
+}
+
+// Per (request i, chunk c):
+//   fold the chunk statistics of the request's rows (one wave per row, fixed
+//   reduction order) into fp64 (M, Z); run the tests of Eq. (1) (one lane per
+//   draft node, against its parent's rows); walk to the deepest accepted node;
+//   the chunk's mass of the final-sample weights.  The last of the request's
+//   work-groups to publish its mass (a device-scope ticket) then samples:
+//   prefix over the chunk masses, the chunk holding u * total, an fp64 scan
+//   inside it, the smallest token id whose cumulative weight exceeds u * total.
 template <typename T>
-__global__ __launch_bounds__(kAccThreads) void acc_decide_mass(AccParams p) {
+__global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   __shared__ double redd[4];
+  __shared__ float s_M[kMaxNodes];
+  __shared__ double s_Z[kMaxNodes];
   __shared__ Decision s_dec;
+  __shared__ int s_last;
+  __shared__ double s_mass[kAccMaxChunks];
+  __shared__ double s_tsum[kAccThreads];
+  __shared__ double s_tot, s_base, s_target;
+  __shared__ int s_chunk;
+  __shared__ int s_cand[4], s_last_pos[4];
   const int i = blockIdx.x / p.nch, c = blockIdx.x % p.nch;
+  const int tid = threadIdx.x, wv = tid >> 6, ln = tid & 63;
   const ReqInfo rq = p.reqs[i];
   const int N = rq.nq;
   const T* L = static_cast<const T*>(p.logits);
   const T* Q = static_cast<const T*>(p.probs);
 
-  if (threadIdx.x < 64) {
+  // Loads the tests need that do not depend on the row statistics, issued
+  // first: each non-root node's token, the parent row's logit and draft
+  // probability at it, and its uniform.
+  const int n = tid;
+  const bool tester = n >= 1 && n < N;      // lanes of wave 0 only (N <= 32)
+  int par = 0;
+  float lx = 0.f, qx = 0.f, un = 0.f;
+  if (tester) {
+    par = node_parent(p, n);
+    const int x = p.tokens[rq.q0 - i + n - 1];
+    lx = ld(L, (int64_t)(rq.q0 + par) * p.l_st + x);
+    qx = ld(Q, (int64_t)(rq.d0 + node_qrank(p, par, N)) * p.p_st + x);
+    un = p.uniforms[rq.q0 + n - 1];
+  }
+
+  // (M, Z) of every row of the request
+  for (int r = wv; r < N; r += kAccThreads / 64) {
+    const ChunkStat* st = p.rowstats + (int64_t)(rq.q0 + r) * p.nch;
+    float m = -INFINITY;
+    for (int k = ln; k < p.nch; k += 64) m = fmaxf(m, st[k].m);
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    double z = 0.0;
+    for (int k = ln; k < p.nch; k += 64) z += st[k].s * exp((double)st[k].m - (double)m);
+    for (int o = 32; o >= 1; o >>= 1) z += __shfl_xor(z, o);
+    if (ln == 0) {
+      s_M[r] = m;
+      s_Z[r] = z;
+    }
+  }
+  __syncthreads();
+
+  if (tid < 64) {
     // one lane per non-root node: the test of Eq. (1) against its parent's rows
-    const int n = threadIdx.x;
     bool pass = false;
-    if (n >= 1 && n < N) {
-      const int par = node_parent(p, n);
-      const int row = rq.q0 + par;
-      float M;
-      double Z;
-      fold_row(p, row, &M, &Z);
-      const int x = p.tokens[rq.q0 - i + n - 1];
-      const double px = exp((double)ld(L, (int64_t)row * p.l_st + x) - (double)M) / Z;
-      const int qr = rq.d0 + node_qrank(p, par, N);
-      const double qx = (double)ld(Q, (int64_t)qr * p.p_st + x);
-      const double u = (double)p.uniforms[rq.q0 + n - 1];
-      pass = u * qx < px;
+    if (tester) {
+      const double px = exp((double)lx - (double)s_M[par]) / s_Z[par];
+      pass = (double)un * (double)qx < px;
     }
     const unsigned long long passmask = __ballot(pass);
     if (n == 0) {
@@ -177,7 +219,8 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_mass(AccParams p) {
       d.row = rq.q0 + best;
       d.qrow = qrank >= 0 ? rq.d0 + qrank : -1;
       d.len = node_depth(p, best);
-      fold_row(p, d.row, &d.M, &d.Z);
+      d.M = s_M[best];
+      d.Z = s_Z[best];
       d.pad = 0.f;
       s_dec = d;
     }
@@ -185,88 +228,85 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_mass(AccParams p) {
   __syncthreads();
   const Decision d = s_dec;
   const double invZ = 1.0 / d.Z;
-  const bool residual = d.qrow >= 0;
-  float x[16], q[16];
-  load16_coalesced(L + (int64_t)d.row * p.l_st, c * kAccChunk, p.V, -INFINITY, x);
-  if (residual) load16_coalesced(Q + (int64_t)d.qrow * p.p_st, c * kAccChunk, p.V, 0.f, q);
-  double s = 0.0;
+  bool residual = d.qrow >= 0;
+  const T* Lr = L + (int64_t)d.row * p.l_st;
+  const T* Qr = Q + (int64_t)(d.qrow >= 0 ? d.qrow : 0) * p.p_st;
+  {
+    float x[16], q[16];
+    load16_coalesced(Lr, c * kAccChunk, p.V, -INFINITY, x);
+    if (residual) load16_coalesced(Qr, c * kAccChunk, p.V, 0.f, q);
+    double sm = 0.0;
 #pragma unroll
-  for (int k = 0; k < 16; ++k) s += final_weight(x[k], residual ? q[k] : 0.f, d.M, invZ, residual);
-  s = block_sum(s, redd);
-  if (threadIdx.x == 0) {
-    p.masses[(int64_t)i * p.nch + c] = s;
-    if (c == 0) p.decision[i] = d;
+    for (int k = 0; k < 16; ++k) sm += final_weight(x[k], residual ? q[k] : 0.f, d.M, invZ, residual);
+    sm = block_sum(sm, redd);
+    if (tid == 0) {
+      if (p.nch == 1) {
+        s_mass[0] = sm;
+        s_last = 1;
+      } else {
+        store_dev(p.masses + (int64_t)i * p.nch + c, sm);
+        __builtin_amdgcn_s_waitcnt(0);     // the store has reached the device coherence point
+        const int t = __hip_atomic_fetch_add(p.tickets + i, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = (t == p.nch - 1);
+      }
+    }
   }
-}
+  __syncthreads();
+  if (!s_last) return;              // uniform: another work-group of the request samples
 
-template <typename T>
-__global__ __launch_bounds__(kAccThreads) void acc_select(AccParams p) {
-  __shared__ double redd[4];
-  __shared__ double s_mass[kAccMaxChunks];
-  __shared__ double s_tsum[kAccThreads];
-  __shared__ double s_tot, s_base, s_target;
-  __shared__ int s_chunk;
-  __shared__ int s_cand[4], s_last[4];
-  const int i = blockIdx.x;
-  const int tid = threadIdx.x;
-  const Decision d = p.decision[i];
-  const double invZ = 1.0 / d.Z;
-  const T* L = static_cast<const T*>(p.logits) + (int64_t)d.row * p.l_st;
-  const T* Q = static_cast<const T*>(p.probs) + (int64_t)(d.qrow >= 0 ? d.qrow : 0) * p.p_st;
-  const float u = p.uniforms[p.reqs[i].q0 + p.reqs[i].nq - 1];
-  const double* masses = p.masses + (int64_t)i * p.nch;
-
+  // ---- the request's sampler
+  if (p.nch > 1)
+    for (int k = tid; k < p.nch; k += kAccThreads) s_mass[k] = load_dev(p.masses + (int64_t)i * p.nch + k);
+  __syncthreads();
   if (tid == 0) {
     double tot = 0.0;
-    for (int c = 0; c < p.nch; ++c) tot += masses[c];
+    for (int k = 0; k < p.nch; ++k) tot += s_mass[k];
     s_tot = tot;
   }
   __syncthreads();
   // zero residual mass (reachable only through rounding): sample from p itself
-  const bool fallback = !(s_tot > 0.0);
-  const bool residual = d.qrow >= 0 && !fallback;
-  if (!fallback) {
-    for (int c = tid; c < p.nch; c += kAccThreads) s_mass[c] = masses[c];
-  } else {
-    for (int c = 0; c < p.nch; ++c) {
+  if (!(s_tot > 0.0)) {
+    residual = false;
+    for (int k = 0; k < p.nch; ++k) {
       float x[16];
-      load16_coalesced(L, c * kAccChunk, p.V, -INFINITY, x);
-      double s = 0.0;
+      load16_coalesced(Lr, k * kAccChunk, p.V, -INFINITY, x);
+      double sm = 0.0;
 #pragma unroll
-      for (int k = 0; k < 16; ++k) s += final_weight(x[k], 0.f, d.M, invZ, false);
-      s = block_sum(s, redd);
-      if (tid == 0) s_mass[c] = s;
+      for (int e = 0; e < 16; ++e) sm += final_weight(x[e], 0.f, d.M, invZ, false);
+      sm = block_sum(sm, redd);
+      if (tid == 0) s_mass[k] = sm;
     }
+    __syncthreads();
   }
-  __syncthreads();
+  const float u = p.uniforms[rq.q0 + N - 1];
   if (tid == 0) {
     double tot = 0.0;
-    for (int c = 0; c < p.nch; ++c) tot += s_mass[c];
+    for (int k = 0; k < p.nch; ++k) tot += s_mass[k];
     const double target = (double)u * tot;
     double cum = 0.0;
     int chosen = -1, last_pos = 0;
-    for (int c = 0; c < p.nch; ++c) {
-      if (s_mass[c] > 0.0) last_pos = c;
+    for (int k = 0; k < p.nch; ++k) {
+      if (s_mass[k] > 0.0) last_pos = k;
       if (chosen < 0) {
-        if (cum + s_mass[c] > target) chosen = c;
-        else cum += s_mass[c];
+        if (cum + s_mass[k] > target) chosen = k;
+        else cum += s_mass[k];
       }
     }
     if (chosen < 0) {   // target rounded past the total: last chunk with mass
       chosen = last_pos;
       cum = 0.0;
-      for (int c = 0; c < chosen; ++c) cum += s_mass[c];
+      for (int k = 0; k < chosen; ++k) cum += s_mass[k];
     }
     s_chunk = chosen;
     s_base = cum;
     s_target = target;
   }
   __syncthreads();
-  const int c = s_chunk;
+  const int cc = s_chunk;
   float x[16], q[16];
   double w[16];
-  load16_contiguous(L, c * kAccChunk, p.V, -INFINITY, x);
-  if (residual) load16_contiguous(Q, c * kAccChunk, p.V, 0.f, q);
+  load16_contiguous(Lr, cc * kAccChunk, p.V, -INFINITY, x);
+  if (residual) load16_contiguous(Qr, cc * kAccChunk, p.V, 0.f, q);
   double tsum = 0.0;
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
@@ -297,7 +337,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_select(AccParams p) {
   double run = s_base + s_tsum[tid];
   const double target = s_target;
   int cand = 0x7fffffff, lastpos = -1;
-  const int v0 = c * kAccChunk + 16 * tid;
+  const int v0 = cc * kAccChunk + 16 * tid;
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
     run += w[k];
@@ -313,12 +353,12 @@ __global__ __launch_bounds__(kAccThreads) void acc_select(AccParams p) {
   }
   if ((tid & 63) == 0) {
     s_cand[tid >> 6] = cand;
-    s_last[tid >> 6] = lastpos;
+    s_last_pos[tid >> 6] = lastpos;
   }
   __syncthreads();
   if (tid == 0) {
     int best = min(min(s_cand[0], s_cand[1]), min(s_cand[2], s_cand[3]));
-    if (best == 0x7fffffff) best = max(max(s_last[0], s_last[1]), max(s_last[2], s_last[3]));
+    if (best == 0x7fffffff) best = max(max(s_last_pos[0], s_last_pos[1]), max(s_last_pos[2], s_last_pos[3]));
     p.next_tok[i] = best;
     p.acc_len[i] = d.len;
     if (p.acc_node) p.acc_node[i] = d.node;
@@ -331,12 +371,10 @@ hipError_t launch_accept(const AccParams& p, hipStream_t s) {
   dim3 block(kAccThreads);
   if (p.bf16) {
     acc_rowstats<uint16_t><<<dim3(p.Nq * p.nch), block, 0, s>>>(p);
-    acc_decide_mass<uint16_t><<<dim3(p.B * p.nch), block, 0, s>>>(p);
-    acc_select<uint16_t><<<dim3(p.B), block, 0, s>>>(p);
+    acc_decide_select<uint16_t><<<dim3(p.B * p.nch), block, 0, s>>>(p);
   } else {
     acc_rowstats<float><<<dim3(p.Nq * p.nch), block, 0, s>>>(p);
-    acc_decide_mass<float><<<dim3(p.B * p.nch), block, 0, s>>>(p);
-    acc_select<float><<<dim3(p.B), block, 0, s>>>(p);
+    acc_decide_select<float><<<dim3(p.B * p.nch), block, 0, s>>>(p);
   }
   return hipGetLastError();
 }

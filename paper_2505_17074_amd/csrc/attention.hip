@@ -571,29 +571,56 @@ __global__ __launch_bounds__(256) void attn_split_valu(AttnParams p) {
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void attn_combine(AttnParams p) {
+  // One wave per (query row, head) of a split request, four per work-group.
+  // Lane s holds partial s's running max and sum (64 partials per pass); the
+  // log-sum-exp weights reach the other lanes by shuffle, and the column sums
+  // run eight partials at a time so their loads overlap.  Fixed order
+  // throughout (bit-reproducible).
   constexpr int PER = D / 64;
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= (int64_t)p.Nq * p.Hq) return;
   const int qrow = (int)(row / p.Hq), h = (int)(row % p.Hq);
   const ReqInfo rq = p.reqs[p.row_req[qrow]];
-  if (rq.nseg <= 1) return;
-  const int j = qrow - rq.q0, n = rq.nq;
+  if (rq.nseg <= 1) return;           // written directly by the split kernel
+  const int j = qrow - rq.q0, n = rq.nq, nseg = rq.nseg;
+  auto prow = [&](int sg) -> int64_t { return rq.part0 + ((int64_t)sg * n + j) * p.Hq + h; };
   float M = -INFINITY;
-  for (int s = 0; s < rq.nseg; ++s)
-    M = fmaxf(M, p.part_ml[rq.part0 + ((int64_t)s * n + j) * p.Hq + h].x);
-  float acc[PER];
+  for (int sg = lane; sg < nseg; sg += 64) M = fmaxf(M, p.part_ml[prow(sg)].x);
+  for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  float acc[PER], L = 0.f;
 #pragma unroll
   for (int x = 0; x < PER; ++x) acc[x] = 0.f;
-  float L = 0.f;
-  for (int s = 0; s < rq.nseg; ++s) {
-    const int64_t pr = rq.part0 + ((int64_t)s * n + j) * p.Hq + h;
-    const float2 ml = p.part_ml[pr];
-    const float w = (ml.x == -INFINITY) ? 0.f : exp2f(ml.x - M);
-    L += ml.y * w;
+  for (int s0 = 0; s0 < nseg; s0 += 64) {
+    float w = 0.f;
+    if (s0 + lane < nseg) {
+      const float2 ml = p.part_ml[prow(s0 + lane)];
+      w = (ml.x == -INFINITY) ? 0.f : exp2f(ml.x - M);
+      float lw = ml.y * w;
+      L += lw;
+    }
+    const int cnt = min(64, nseg - s0);
+    int k = 0;
+    for (; k + 8 <= cnt; k += 8) {
+      float v[8][PER];
 #pragma unroll
-    for (int x = 0; x < PER; ++x) acc[x] += w * p.part_o[pr * D + lane + 64 * x];
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int x = 0; x < PER; ++x) v[u][x] = p.part_o[prow(s0 + k + u) * D + lane + 64 * x];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float wu = __shfl(w, k + u);
+#pragma unroll
+        for (int x = 0; x < PER; ++x) acc[x] += wu * v[u][x];
+      }
+    }
+    for (; k < cnt; ++k) {
+      const float wu = __shfl(w, k);
+#pragma unroll
+      for (int x = 0; x < PER; ++x) acc[x] += wu * p.part_o[prow(s0 + k) * D + lane + 64 * x];
+    }
   }
+  for (int o = 32; o >= 1; o >>= 1) L += __shfl_xor(L, o);
   const float inv = 1.f / L;
 #pragma unroll
   for (int x = 0; x < PER; ++x) p.out[((int64_t)qrow * p.Hq + h) * D + lane + 64 * x] = acc[x] * inv;

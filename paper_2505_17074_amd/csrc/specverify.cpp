@@ -41,7 +41,7 @@ struct Plan {
   int nch = 0;
   // layout (bytes)
   size_t off_topo = 0, off_reqs = 0, off_items = 0, off_rowreq = 0, plan_bytes = 0;
-  size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_decision = 0, off_masses = 0;
+  size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_masses = 0, off_tickets = 0;
   size_t device_bytes = 0;
 };
 
@@ -102,19 +102,48 @@ spec_status_t check_accept(const spec_accept_args_t* a, int64_t Nq, int B) {
   return SPEC_OK;
 }
 
-// Keys per split.  With fewer (request, KV head, head group) streams than the
-// chip has compute units, streams are cut for parallelism alone (~1536
-// pieces).  Otherwise pieces aim at ~2048 items for load balance across
-// ragged lengths, but stay >= 40 * rows so the fp32 partials (rows x d x 4
-// bytes, written once and read once by the combine) remain a few percent of
-// the K/V bytes a piece streams (32 rows x d x 2 x 2 per 32 keys).
-int auto_split(int64_t key_streams, int64_t streams, int rows_max) {
-  int64_t s;
-  if (streams < 256) {
-    s = (key_streams + 1535) / 1536;
-  } else {
-    s = std::max<int64_t>((key_streams + 2047) / 2048, 40 * (int64_t)rows_max);
+// Compute units of the current device (cached; 256 when it cannot be asked,
+// e.g. for a size query on a host without a GPU).
+int device_cus() {
+  static int cus[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return 256;
   }
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+      (void)hipGetLastError();
+      n = 256;
+    }
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
+// Work-groups of the bf16 split kernel one compute unit holds, by waves per
+// work-group (registers and LDS of the d = 128 build, as measured).
+int groups_per_cu(int waves) {
+  static const int table[6] = {0, 3, 3, 2, 2, 1};
+  return table[std::min(std::max(waves, 1), 5)];
+}
+
+// Keys per split piece.  `slots` = work-groups the device runs at once.
+// Pieces are at most kMaxPiece keys: a longer item, started first, still
+// outlasts the rest of the kernel once the other work-groups have drained
+// (measured on ragged batches: 6464-key pieces 28% slower than 4096).  With
+// fewer (request, KV head, head group) streams than slots, pieces shrink to
+// about one per slot.  They stay >= 40 * rows keys, so the fp32 partials
+// (rows x d x 4 bytes, written once and read once by the combine) remain a
+// few percent of the K/V bytes a piece streams (32 rows x d x 2 x 2 per 32
+// keys), and >= 256 keys.
+constexpr int64_t kMaxPiece = 4096;
+int auto_split(int64_t key_streams, int64_t streams, int rows_max, int64_t slots) {
+  slots = std::max<int64_t>(slots, 1);
+  int64_t s = kMaxPiece;
+  if (streams < slots) s = std::min<int64_t>(s, (key_streams + slots - 1) / slots);
+  s = std::max<int64_t>(s, 40 * (int64_t)rows_max);
   s = std::max<int64_t>(s, 256);
   s = (s + 31) / 32 * 32;
   return (int)std::min<int64_t>(s, 1 << 20);
@@ -208,7 +237,8 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
       nstreams += (int64_t)Hkv * groups[i];
       rows_max = std::max(rows_max, hpg[i] * n);
     }
-    P.split = attn->split_kv > 0 ? attn->split_kv : auto_split(streams, nstreams, rows_max);
+    const int64_t slots = (int64_t)device_cus() * (bf ? groups_per_cu((rows_max + 15) / 16) : 2);
+    P.split = attn->split_kv > 0 ? attn->split_kv : auto_split(streams, nstreams, rows_max, slots);
     int64_t part = 0;
     int nr = 1;
     for (int i = 0; i < P.B; ++i) {
@@ -265,6 +295,8 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   off = align_up(off + sizeof(AttnItem) * P.items.size());
   P.off_rowreq = off;
   off = align_up(off + sizeof(int32_t) * P.Nq);
+  P.off_tickets = off;                 // acceptance tickets, uploaded as zero
+  off = align_up(off + sizeof(int32_t) * (size_t)(P.has_acc ? P.B : 0));
   P.plan_bytes = off;
   const int D = attn ? attn->head_dim : 0;
   P.off_part_o = off;
@@ -273,8 +305,6 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   off = align_up(off + sizeof(float) * 2 * (size_t)P.parts);
   P.off_rowstats = off;
   off = align_up(off + sizeof(sv::ChunkStat) * (size_t)(P.has_acc ? P.Nq * P.nch : 0));
-  P.off_decision = off;
-  off = align_up(off + sizeof(sv::Decision) * (size_t)(P.has_acc ? P.B : 0));
   P.off_masses = off;
   off = align_up(off + sizeof(double) * (size_t)(P.has_acc ? (int64_t)P.B * P.nch : 0));
   P.device_bytes = off;
@@ -386,7 +416,7 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     c.topo = topo;
     c.row_req = row_req;
     c.rowstats = reinterpret_cast<sv::ChunkStat*>(d + P.off_rowstats);
-    c.decision = reinterpret_cast<sv::Decision*>(d + P.off_decision);
+    c.tickets = reinterpret_cast<int32_t*>(d + P.off_tickets);
     c.masses = reinterpret_cast<double*>(d + P.off_masses);
     c.V = acc->vocab;
     c.nch = P.nch;

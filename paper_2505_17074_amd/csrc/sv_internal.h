@@ -99,8 +99,8 @@ struct AccParams {
   const Topo* topo;
   const int32_t* row_req;
   ChunkStat* rowstats;   // [Nq, nch]
-  Decision* decision;    // [B]
   double* masses;        // [B, nch] final-sample weight mass per chunk
+  int32_t* tickets;      // [B] chunk masses published per request (zero at launch: uploaded with the plan)
   int32_t V, nch, B, Nq;
   int32_t tree;        // 1 = tree mode
   int32_t bf16;
