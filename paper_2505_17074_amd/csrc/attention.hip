@@ -65,8 +65,11 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // Ring depth (tiles in LDS) by waves per work-group.  Fewer work-groups fit on
 // a compute unit as W grows (registers), so deeper rings keep enough bytes in
 // flight per compute unit.
+#ifndef SV_WPE_W34
+#define SV_WPE_W34 1
+#endif
 #ifndef SV_NS_W1
-#define SV_NS_W1 3
+#define SV_NS_W1 4
 #endif
 #ifndef SV_NS_W2
 #define SV_NS_W2 3
@@ -309,8 +312,18 @@ struct AttnLds {
   static constexpr int BYTES = MAIN > QEND ? MAIN : QEND;
 };
 
+// Register budget by waves per work-group.  A 5-wave work-group is placed only
+// where every SIMD can take two of its waves, so a second one per compute unit
+// needs <= 128 registers (measured: long-context GQA 17% faster).  Bounding
+// 3-4 waves to 168 (three work-groups per compute unit) measured neutral.
+template <int W>
+struct WavesPerEu {
+  static constexpr int value = W == 5 ? 4 : (W >= 3 ? SV_WPE_W34 : 1);
+};
+
 template <int D, int W, int NS>
-__global__ __launch_bounds__(64 * W) void attn_split_mfma(AttnParams p) {
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(WavesPerEu<W>::value)))
+void attn_split_mfma(AttnParams p) {
   using G = Geo<D>;
   constexpr int ET = D / 16, KS = D / 32;
   constexpr int PER = Xfer<D, W>::PER;

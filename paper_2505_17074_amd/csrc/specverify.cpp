@@ -441,7 +441,10 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     return true;
   };
 
-  if (attn && acc) {
+#ifndef SV_OVERLAP
+#define SV_OVERLAP 1
+#endif
+  if (SV_OVERLAP && attn && acc) {
     SideStream* S = side_stream();
     if (!S) return SPEC_ERR_HIP;
     std::lock_guard<std::mutex> lk(S->mu);
