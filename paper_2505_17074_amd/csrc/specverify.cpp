@@ -241,6 +241,12 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
     P.split = attn->split_kv > 0 ? attn->split_kv : auto_split(streams, nstreams, rows_max, slots);
     int64_t part = 0;
     int nr = 1;
+    {
+      int64_t n_items = 0;
+      for (int i = 0; i < P.B; ++i)
+        n_items += ((int64_t)P.reqs[i].ctx + P.reqs[i].nq + P.split - 1) / P.split * Hkv * groups[i];
+      P.items.reserve((size_t)n_items);
+    }
     for (int i = 0; i < P.B; ++i) {
       ReqInfo& q = P.reqs[i];
       const int L = q.ctx + q.nq;
@@ -276,10 +282,18 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
     }
     // Longest items first: work-groups are dispatched in index order as slots
     // free up, so the last ones to start are the shortest and the kernel's
-    // tail (slots idling while a few long items finish) stays short.
-    std::stable_sort(P.items.begin(), P.items.end(), [](const AttnItem& x, const AttnItem& y) {
-      return (x.ke - x.kb + 31) / 32 > (y.ke - y.kb + 31) / 32;
-    });
+    // tail (slots idling while a few long items finish) stays short.  A
+    // stable counting sort on the tile count (linear in the item count).
+    {
+      int max_t = 0;
+      for (const AttnItem& it : P.items) max_t = std::max(max_t, (it.ke - it.kb + 31) / 32);
+      std::vector<int> start(max_t + 2, 0);
+      for (const AttnItem& it : P.items) ++start[max_t - (it.ke - it.kb + 31) / 32 + 1];
+      for (int t = 1; t <= max_t + 1; ++t) start[t] += start[t - 1];
+      std::vector<AttnItem> sorted(P.items.size());
+      for (const AttnItem& it : P.items) sorted[start[max_t - (it.ke - it.kb + 31) / 32]++] = it;
+      P.items.swap(sorted);
+    }
     if (part >= INT32_MAX) return SPEC_ERR_INVALID_ARG;
     P.parts = part;
     P.nr_max = nr;
@@ -342,7 +356,9 @@ SideStream* side_stream() {
 
 void write_staging(const Plan& P, void* host) {
   char* h = static_cast<char*>(host);
-  std::memset(h, 0, P.plan_bytes);
+  // every section is written whole; the acceptance tickets must start at
+  // zero (alignment padding between sections is never read)
+  std::memset(h + P.off_tickets, 0, P.plan_bytes - P.off_tickets);
   std::memcpy(h + P.off_topo, &P.topo, sizeof(Topo));
   std::memcpy(h + P.off_reqs, P.reqs.data(), sizeof(ReqInfo) * P.reqs.size());
   if (!P.items.empty()) std::memcpy(h + P.off_items, P.items.data(), sizeof(AttnItem) * P.items.size());
