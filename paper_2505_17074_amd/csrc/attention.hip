@@ -9,6 +9,7 @@
 #include "sv_internal.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace sv {
 namespace {
@@ -62,9 +63,11 @@ __device__ __forceinline__ bool visible(int t, int ctx, uint32_t anc) {
 // 16e + i.  The item's output is staged through LDS and written as rows.
 // ---------------------------------------------------------------------------
 typedef __attribute__((address_space(3))) void lds_void_t;
-// Ring depth (tiles in LDS) by waves per work-group.  Fewer work-groups fit on
-// a compute unit as W grows (registers), so deeper rings keep enough bytes in
-// flight per compute unit.
+// Ring depth (tiles in LDS) by waves per work-group, as measured.  A 4-stage
+// ring (64 KB) keeps two work-groups of one to three waves per compute unit
+// with three tiles each in flight.  A 5-wave work-group loses its second slot
+// per compute unit once it holds 56 KB of LDS (long-context GQA 28% slower),
+// so W = 5 stays at three stages (48 KB); W = 4 measured 1-2% faster at three.
 #ifndef SV_WPE_W34
 #define SV_WPE_W34 1
 #endif
@@ -72,10 +75,10 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 #define SV_NS_W1 4
 #endif
 #ifndef SV_NS_W2
-#define SV_NS_W2 3
+#define SV_NS_W2 4
 #endif
 #ifndef SV_NS_W3
-#define SV_NS_W3 3
+#define SV_NS_W3 4
 #endif
 #ifndef SV_NS_W4
 #define SV_NS_W4 3
@@ -115,6 +118,15 @@ template <int N>
 __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// f(integral_constant<int, I>) for I = B .. E-1, in order.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
 }
 
 // Work-group barrier for the tile ring.  __syncthreads() is a release fence at
@@ -197,10 +209,14 @@ struct RowTile {
   float m, l;
 };
 
-template <int D>
-__device__ __forceinline__ void compute_tile(const char* stage, RowTile<D>& S, int t0, int ke, int ctx,
+// Tile compute on ring stage SOFF / STAGE (a compile-time byte offset into
+// `ring`), so every LDS read of the stage carries its offset as an immediate
+// and the per-lane address registers are shared by all stages.
+template <int D, int SOFF>
+__device__ __forceinline__ void compute_tile(const char* ring, RowTile<D>& S, int t0, int ke, int ctx,
                                              float scale_log2, int lane) {
   using G = Geo<D>;
+  const char* stage = ring + SOFF;
   constexpr int KS = D / 32, ET = D / 16;
   const int grp = lane >> 4;
   f32x4 s[2];
@@ -275,17 +291,22 @@ __device__ __forceinline__ void compute_tile(const char* stage, RowTile<D>& S, i
   // reads are issued from inline assembly with their own lgkmcnt waits: the
   // compiler's builtin for this read makes it wait for every outstanding
   // LDS-bound transfer (vmcnt(0)), which would serialise the ring.
-  const uint32_t vbase = (uint32_t)(uintptr_t)(stage + G::MAT);
+  // The stage's V offset goes into the instructions' 16-bit immediate where
+  // it fits (S.voff holds the ring's LDS address plus the lane offset).
+  constexpr int VOFF = SOFF + G::MAT;
+  constexpr bool IMM = VOFF + 4 * G::ROWB <= 65535;
+  const uint32_t vadd = IMM ? 0u : (uint32_t)VOFF;
+  constexpr int I0 = IMM ? VOFF : 0;
   constexpr int VG = 4;
 #pragma unroll
   for (int e0 = 0; e0 < ET; e0 += VG) {
     s16x4 lo[VG], hi[VG];
 #pragma unroll
     for (int e = 0; e < VG; ++e) {
-      const uint32_t a = vbase + (uint32_t)S.voff[e0 + e];
-      asm volatile("ds_read_b64_tr_b16 %0, %2\n\tds_read_b64_tr_b16 %1, %2 offset:%3"
+      const uint32_t a = S.voff[e0 + e] + vadd;
+      asm volatile("ds_read_b64_tr_b16 %0, %2 offset:%3\n\tds_read_b64_tr_b16 %1, %2 offset:%4"
                    : "=&v"(lo[e]), "=&v"(hi[e])   // early clobber: the address is read twice
-                   : "v"(a), "i"(4 * G::ROWB));
+                   : "v"(a), "i"(I0), "i"(I0 + 4 * G::ROWB));
     }
     asm volatile("s_waitcnt lgkmcnt(0)"
                  : "+v"(lo[0]), "+v"(hi[0]), "+v"(lo[1]), "+v"(hi[1]), "+v"(lo[2]), "+v"(hi[2]), "+v"(lo[3]),
@@ -303,13 +324,7 @@ template <int D, int W, int NS>
 struct AttnLds {
   static constexpr int RING = NS * Geo<D>::STAGE;
   static constexpr int OUT = W * 16 * (D + 4) * 4;  // fp32 output staging, padded rows
-  static constexpr int MAIN = RING > OUT ? RING : OUT;
-  // The query rows (16 bf16 rows per wave) sit in the ring's last stage, which
-  // the first tile transfer into it only overwrites after the first barrier.
-  static constexpr int QT = 16 * Geo<D>::ROWB;
-  static constexpr int QOFF = (NS - 1) * Geo<D>::STAGE;
-  static constexpr int QEND = QOFF + W * QT;
-  static constexpr int BYTES = MAIN > QEND ? MAIN : QEND;
+  static constexpr int BYTES = RING > OUT ? RING : OUT;
 };
 
 // Register budget by waves per work-group.  A 5-wave work-group is placed only
@@ -345,20 +360,19 @@ void attn_split_mfma(AttnParams p) {
   const int range = (it.ctx + it.nq) * row_bytes;
   const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)Kb, 0, range, 0x00020000);
   const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)Vb, 0, range, 0x00020000);
-  char* qlds = lds + AttnLds<D, W, NS>::QOFF + w * AttnLds<D, W, NS>::QT;
-
-  // This wave's 16 query rows go HBM -> LDS with the same direct transfers as
-  // K/V (no register loads are pending when the tile loop starts, so nothing
-  // waits on more than the oldest tile).  Padding rows repeat the item's row 0.
-#pragma unroll
-  for (int jj = 0; jj < 16 / G::RPI; ++jj) {
-    const int rl = jj * G::RPI + lane / G::CH;
-    int rr = w * 16 + rl;
+  RowTile<D> S;
+  // This lane's B operand of the score product straight from HBM: query row
+  // 16w + c16 (padding rows repeat the item's row 0), columns 32ks + 8grp ..
+  // +7.  These loads are older than every tile transfer, so the wait after
+  // the ring's prologue below covers them without draining the ring.
+  {
+    int rr = w * 16 + c16;
     if (rr >= R) rr = 0;
     const int hh = rr / n, j = rr - hh * n;
     const char* src = static_cast<const char*>(p.q) +
-                      ((int64_t)(it.q0 + j) * p.q_st + (int64_t)(it.head_lo + hh) * p.q_sh) * 2 + (lane % G::CH) * 16;
-    __builtin_amdgcn_global_load_lds(src, (lds_void_t*)(qlds + jj * 1024), 16, 0, 0);
+                      ((int64_t)(it.q0 + j) * p.q_st + (int64_t)(it.head_lo + hh) * p.q_sh) * 2 + grp * 16;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) S.q[ks] = *reinterpret_cast<const bf16x8*>(src + ks * 64);
   }
 
   XferPlan<D, W> X;
@@ -368,7 +382,6 @@ void attn_split_mfma(AttnParams p) {
     X.off[q] = xfer_offset<D>((w + q * W) % Xfer<D, W>::NI, lane, row_bytes, &row);
   }
 
-  RowTile<D> S;
   {
     const int r = w * 16 + c16;
     const int j = (r < R) ? r % n : -1;
@@ -389,42 +402,45 @@ void attn_split_mfma(AttnParams p) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) S.koff[ks] = rk0 * G::ROWB + (((ks * 4 + grp) ^ swk<D>(rk0)) * 16);
     const int rv0 = 8 * grp + (c16 >> 2);
+    const uint32_t ring_lds = (uint32_t)(uintptr_t)lds;
 #pragma unroll
     for (int et = 0; et < ET; ++et)
-      S.voff[et] = rv0 * G::ROWB + (((2 * et + ((c16 & 3) >> 1)) ^ swv<D>(rv0)) * 16) + (c16 & 1) * 8;
+      S.voff[et] = ring_lds + rv0 * G::ROWB + (((2 * et + ((c16 & 3) >> 1)) ^ swv<D>(rv0)) * 16) + (c16 & 1) * 8;
   }
   const bool active = w * 16 < R;     // wave-uniform: this wave has query rows
 
-  // the ring's first NS-1 tiles (only tiles of the item are ever transferred)
+  // The ring's first NS-1 tiles, issued whatever the item's length so that
+  // every wave has the same transfer count behind its query loads (a tile
+  // past the item's end re-reads its last key row, in bounds, and is never
+  // computed).  The query loads are older than these transfers: wait for them
+  // alone, and hand the registers through an empty asm so that no later use
+  // inherits a wait on the ring.
 #pragma unroll
   for (int st = 0; st < NS - 1; ++st)
-    if (st < ntiles) issue_tile<D, W>(lds + st * G::STAGE, rk, rv, row_bytes, it.kb + 32 * st, it.ke, w, lane, X);
-
-  // The query rows are this wave's oldest transfers, so they have landed once
-  // the first tile's wait passes; they are read before the first barrier, after
-  // which stage NS-1 is refilled.
-  bool have_q = false;
-  for (int tb = 0; tb < ntiles; tb += NS) {
+    issue_tile<D, W>(lds + st * G::STAGE, rk, rv, row_bytes, it.kb + 32 * st, it.ke, w, lane, X);
+  wait_vm<PER * (NS - 1)>();
 #pragma unroll
-    for (int st = 0; st < NS; ++st) {           // stage index is a compile-time constant
+  for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(S.q[ks]));
+
+  for (int tb = 0; tb < ntiles; tb += NS) {
+    bool stop = false;
+    static_for<0, NS>([&](auto stc) {             // stage index is a compile-time constant
+      constexpr int st = decltype(stc)::value;
       const int t = tb + st;
-      if (t >= ntiles) break;
+      if (stop || t >= ntiles) {
+        stop = true;
+        return;
+      }
       // this wave's transfers of tile t have landed: NS-2 later tiles may still
       // be in flight, none in the item's last NS-2 tiles (over-waiting there)
       if (t + NS - 2 < ntiles) wait_vm<PER * (NS - 2)>();
       else wait_vm<0>();
-      if (!have_q) {
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          S.q[ks] = *reinterpret_cast<const bf16x8*>(qlds + c16 * G::ROWB + (ks * 4 + grp) * 16);
-        have_q = true;
-      }
       ring_barrier();                 // everyone's have landed; stage (t-1) % NS is free
       if (t + NS - 1 < ntiles)
         issue_tile<D, W>(lds + ((st + NS - 1) % NS) * G::STAGE, rk, rv, row_bytes, it.kb + 32 * (t + NS - 1), it.ke,
                          w, lane, X);
-      if (active) compute_tile<D>(lds + st * G::STAGE, S, it.kb + 32 * t, it.ke, ctx, p.scale_log2, lane);
-    }
+      if (active) compute_tile<D, st * G::STAGE>(lds, S, it.kb + 32 * t, it.ke, ctx, p.scale_log2, lane);
+    });
   }
   wait_vm<0>();
   __syncthreads();                    // ring no longer read: reuse it for the output
