@@ -113,6 +113,11 @@ EDGE = [
     ("vocab_5000_bf16_logits", dict(ctx=[10, 20, 30, 40], k=[4, 3, 2, 1], V=5000, logit=W.BF16)),
     ("vocab_tail_f32", dict(ctx=[10, 20], k=[4, 8], V=4100)),
     ("long_single", dict(ctx=[20000], k=[5])),
+    # bf16 kernel widths: at most 32 rows per item -> two waves (one split
+    # request so the combine runs too), at d = 128 and d = 64; 36 rows -> three
+    ("gqa_two_waves_d128", dict(ctx=[300, 1200, 40, 5000], k=[5, 7, 3, 7], Hq=8, Hkv=2)),
+    ("gqa_two_waves_d64", dict(ctx=[100, 2500], k=[7, 2], Hq=8, Hkv=2, d=64)),
+    ("gqa_three_waves_short", dict(ctx=[33, 65, 0], k=[8, 1, 2], Hq=8, Hkv=2)),
 ]
 
 
