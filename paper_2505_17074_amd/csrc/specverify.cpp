@@ -347,8 +347,13 @@ SideStream* side_stream() {
   std::lock_guard<std::mutex> lk(S.mu);
   if (!S.ready) {
     if (hipStreamCreateWithFlags(&S.s, hipStreamNonBlocking) != hipSuccess) return nullptr;
-    if (hipEventCreateWithFlags(&S.fork, hipEventDisableTiming) != hipSuccess) return nullptr;
-    if (hipEventCreateWithFlags(&S.join, hipEventDisableTiming) != hipSuccess) return nullptr;
+    // The pair only orders kernels of two streams on this device; every kernel
+    // dispatch carries its own acquire and release fences, so the events skip
+    // the system-scope fence (host visibility), which costs each step a
+    // cache write-back (measured 1-3% of a step).
+    constexpr unsigned kEv = hipEventDisableTiming | hipEventDisableSystemFence;
+    if (hipEventCreateWithFlags(&S.fork, kEv) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&S.join, kEv) != hipSuccess) return nullptr;
     S.ready = true;
   }
   return &S;
