@@ -602,10 +602,13 @@ template <int D>
 __global__ __launch_bounds__(256) void attn_combine(AttnParams p) {
   // One wave per (query row, head) of a split request, four per work-group.
   // Lane s holds partial s's running max and sum (64 partials per pass); the
-  // log-sum-exp weights reach the other lanes by shuffle, and the column sums
-  // run eight partials at a time so their loads overlap.  Fixed order
-  // throughout (bit-reproducible).
-  constexpr int PER = D / 64;
+  // log-sum-exp weights reach the other lanes by shuffle.  The column sums
+  // take the partial rows eight at a time (a short last group is padded with
+  // a repeated row of weight zero), and the first eight rows are requested
+  // together with the (max, sum) pairs, since they do not depend on the
+  // weights, so a request of up to eight pieces costs one round trip.  Fixed
+  // order throughout (bit-reproducible).
+  constexpr int PER = D / 64, G8 = 8;
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= (int64_t)p.Nq * p.Hq) return;
@@ -614,39 +617,40 @@ __global__ __launch_bounds__(256) void attn_combine(AttnParams p) {
   if (rq.nseg <= 1) return;           // written directly by the split kernel
   const int j = qrow - rq.q0, n = rq.nq, nseg = rq.nseg;
   auto prow = [&](int sg) -> int64_t { return rq.part0 + ((int64_t)sg * n + j) * p.Hq + h; };
-  float M = -INFINITY;
-  for (int sg = lane; sg < nseg; sg += 64) M = fmaxf(M, p.part_ml[prow(sg)].x);
+  auto load_group = [&](int k, float (&v)[G8][PER]) {
+#pragma unroll
+    for (int u = 0; u < G8; ++u)
+#pragma unroll
+      for (int x = 0; x < PER; ++x) v[u][x] = p.part_o[prow(min(k + u, nseg - 1)) * D + lane + 64 * x];
+  };
+  float v[G8][PER];
+  load_group(0, v);
+  float2 ml0 = make_float2(-INFINITY, 0.f);
+  if (lane < nseg) ml0 = p.part_ml[prow(lane)];
+  float M = ml0.x;
+  for (int sg = 64 + lane; sg < nseg; sg += 64) M = fmaxf(M, p.part_ml[prow(sg)].x);
   for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
   float acc[PER], L = 0.f;
 #pragma unroll
   for (int x = 0; x < PER; ++x) acc[x] = 0.f;
   for (int s0 = 0; s0 < nseg; s0 += 64) {
+    const float2 ml = s0 == 0 ? ml0 : (s0 + lane < nseg ? p.part_ml[prow(s0 + lane)] : make_float2(-INFINITY, 0.f));
     float w = 0.f;
     if (s0 + lane < nseg) {
-      const float2 ml = p.part_ml[prow(s0 + lane)];
       w = (ml.x == -INFINITY) ? 0.f : exp2f(ml.x - M);
-      float lw = ml.y * w;
-      L += lw;
+      L += ml.y * w;
     }
     const int cnt = min(64, nseg - s0);
-    int k = 0;
-    for (; k + 8 <= cnt; k += 8) {
-      float v[8][PER];
+    for (int k = 0; k < cnt; k += G8) {
+      if (s0 + k > 0) load_group(s0 + k, v);
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
+      for (int u = 0; u < G8; ++u) {
+        const float wu = __shfl(w, min(k + u, 63));
+        if (k + u < cnt) {
 #pragma unroll
-        for (int x = 0; x < PER; ++x) v[u][x] = p.part_o[prow(s0 + k + u) * D + lane + 64 * x];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float wu = __shfl(w, k + u);
-#pragma unroll
-        for (int x = 0; x < PER; ++x) acc[x] += wu * v[u][x];
+          for (int x = 0; x < PER; ++x) acc[x] += wu * v[u][x];
+        }
       }
-    }
-    for (; k < cnt; ++k) {
-      const float wu = __shfl(w, k);
-#pragma unroll
-      for (int x = 0; x < PER; ++x) acc[x] += wu * p.part_o[prow(s0 + k) * D + lane + 64 * x];
     }
   }
   for (int o = 32; o >= 1; o >>= 1) L += __shfl_xor(L, o);
