@@ -36,8 +36,16 @@
  *     workspaces and staging buffers.
  *   - All argument checks run on the host before any HIP call; on an error
  *     nothing is enqueued and no output is touched.  Device-resident values
- *     (token ids in [0, V), uniforms in [0, 1), finite logits) are the
- *     caller's contract and are not checked.
+ *     (draft token ids in [0, V), uniforms in [0, 1), a positive draft
+ *     probability at each draft token, finite logits) are the caller's
+ *     contract.  They are not checked unless the environment variable
+ *     SPEC_DEBUG_VALIDATE is set to a non-empty value other than "0": then
+ *     spec_accept and spec_verify first check the first three on the device,
+ *     wait for `stream`, and return SPEC_ERR_INVALID_ARG if any fails (the
+ *     plan upload and the check are then the only work enqueued, and no
+ *     output is touched).  Without the check an out-of-range token id is
+ *     clamped into [0, V): its results are meaningless, but nothing outside
+ *     the arguments is read.
  *   - Results are deterministic: the same inputs give bit-identical outputs
  *     (fixed reduction orders, no floating-point atomics).
  */

@@ -173,7 +173,8 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   float lx = 0.f, qx = 0.f, un = 0.f;
   if (tester) {
     par = node_parent(p, n);
-    const int x = p.tokens[rq.q0 - i + n - 1];
+    // an out-of-range id (the caller's contract) is clamped: no read leaves the row
+    const int x = min(max(p.tokens[rq.q0 - i + n - 1], 0), p.V - 1);
     lx = ld(L, (int64_t)(rq.q0 + par) * p.l_st + x);
     qx = ld(Q, (int64_t)(rq.d0 + node_qrank(p, par, N)) * p.p_st + x);
     un = p.uniforms[rq.q0 + n - 1];
@@ -365,7 +366,39 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   }
 }
 
+// One work-group: every request's draft tokens, their draft probabilities
+// and the uniforms, against the caller's contract (debug builds of a call).
+template <typename T>
+__global__ __launch_bounds__(kAccThreads) void acc_validate(AccParams p, uint32_t* flag) {
+  if (threadIdx.x == 0) *flag = 0u;
+  __syncthreads();
+  uint32_t bad = 0u;
+  const T* Q = static_cast<const T*>(p.probs);
+  for (int i = threadIdx.x; i < p.B; i += kAccThreads) {
+    const ReqInfo rq = p.reqs[i];
+    for (int n = 0; n < rq.nq; ++n) {
+      const float u = p.uniforms[rq.q0 + n];
+      if (!(u >= 0.f && u < 1.f)) bad |= 2u;
+      if (n == 0) continue;
+      const int x = p.tokens[rq.q0 - i + n - 1];
+      if (x < 0 || x >= p.V) {
+        bad |= 1u;
+        continue;
+      }
+      const float qx = ld(Q, (int64_t)(rq.d0 + node_qrank(p, node_parent(p, n), rq.nq)) * p.p_st + x);
+      if (!(qx > 0.f)) bad |= 4u;
+    }
+  }
+  if (bad) atomicOr(flag, bad);
+}
+
 }  // namespace
+
+hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_t s) {
+  if (p.bf16) acc_validate<uint16_t><<<1, kAccThreads, 0, s>>>(p, flag);
+  else acc_validate<float><<<1, kAccThreads, 0, s>>>(p, flag);
+  return hipGetLastError();
+}
 
 hipError_t launch_accept(const AccParams& p, hipStream_t s) {
   dim3 block(kAccThreads);

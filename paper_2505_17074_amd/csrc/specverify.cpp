@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <vector>
@@ -41,7 +42,7 @@ struct Plan {
   int nch = 0;
   // layout (bytes)
   size_t off_topo = 0, off_reqs = 0, off_items = 0, off_rowreq = 0, plan_bytes = 0;
-  size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_masses = 0, off_tickets = 0;
+  size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_masses = 0, off_tickets = 0, off_flag = 0;
   size_t device_bytes = 0;
 };
 
@@ -100,6 +101,12 @@ spec_status_t check_accept(const spec_accept_args_t* a, int64_t Nq, int B) {
   if (a->draft_probs && (a->probs_stride < a->vocab || a->probs_stride % vec || !aligned16(a->draft_probs)))
     return SPEC_ERR_INVALID_ARG;
   return SPEC_OK;
+}
+
+// SPEC_DEBUG_VALIDATE set to a non-empty value other than "0" (read per call).
+bool debug_validate() {
+  const char* e = std::getenv("SPEC_DEBUG_VALIDATE");
+  return e && e[0] && !(e[0] == '0' && e[1] == 0);
 }
 
 // Compute units of the current device (cached; 256 when it cannot be asked,
@@ -321,6 +328,8 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   off = align_up(off + sizeof(sv::ChunkStat) * (size_t)(P.has_acc ? P.Nq * P.nch : 0));
   P.off_masses = off;
   off = align_up(off + sizeof(double) * (size_t)(P.has_acc ? (int64_t)P.B * P.nch : 0));
+  P.off_flag = off;                    // debug check result (SPEC_DEBUG_VALIDATE)
+  off = align_up(off + (P.has_acc ? sizeof(uint32_t) : 0));
   P.device_bytes = off;
   return SPEC_OK;
 }
@@ -445,6 +454,17 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     c.Nq = (int32_t)P.Nq;
     c.tree = P.tree ? 1 : 0;
     c.bf16 = acc->dtype == SPEC_BF16;
+  }
+
+  // Optional device check of the acceptance inputs (the caller's contract),
+  // before anything that writes an output is enqueued.
+  if (acc && debug_validate()) {
+    uint32_t* dflag = reinterpret_cast<uint32_t*>(d + P.off_flag);
+    uint32_t hflag = 0;
+    if (sv::launch_accept_validate(c, dflag, s) != hipSuccess) return SPEC_ERR_HIP;
+    if (hipMemcpyAsync(&hflag, dflag, sizeof(hflag), hipMemcpyDeviceToHost, s) != hipSuccess) return SPEC_ERR_HIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return SPEC_ERR_HIP;
+    if (hflag != 0) return SPEC_ERR_INVALID_ARG;
   }
 
   auto launch_acc = [&](hipStream_t st) -> bool {

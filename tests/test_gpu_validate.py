@@ -1,0 +1,94 @@
+"""The optional device check of the acceptance inputs (SPEC_DEBUG_VALIDATE).
+
+With the environment variable set, spec_accept and spec_verify check the
+draft token ids, the uniforms and the draft probability at each draft token
+on the device, and return SPEC_ERR_INVALID_ARG before anything that writes an
+output is enqueued.  Every case here keeps the bad value inside the arguments'
+own buffers, so nothing reads outside them.
+"""
+import numpy as np
+import pytest
+import torch
+
+import parity_util as U
+from paper_2505_17074_amd import binding as B
+from paper_2505_17074_amd.batch import DeviceBatch, Verifier
+
+pytestmark = pytest.mark.gpu
+
+SENTINEL = -7
+
+
+def _pool():
+    return U.custom_pool(ctx=[40, 7, 120], k=[3, 1, 5], Hq=8, Hkv=2, V=3000, seed=11)
+
+
+def _fill_outputs(b):
+    b.accepted_len.fill_(SENTINEL)
+    b.next_token.fill_(SENTINEL)
+    b.accepted_node.fill_(SENTINEL)
+    b.out.fill_(float("nan"))
+
+
+def _untouched(b, attn=True):
+    torch.cuda.synchronize()
+    assert (b.accepted_len.cpu().numpy() == SENTINEL).all()
+    assert (b.next_token.cpu().numpy() == SENTINEL).all()
+    assert (b.accepted_node.cpu().numpy() == SENTINEL).all()
+    if attn:
+        assert torch.isnan(b.out).all().item()
+
+
+def test_valid_inputs_pass_and_match(gpu_lib, monkeypatch):
+    print("[case] validation on, valid inputs", flush=True)
+    pool = _pool()
+    b = DeviceBatch(pool, "cuda")
+    v = Verifier(b)
+    v.run("verify")
+    ref = v.results()
+    monkeypatch.setenv("SPEC_DEBUG_VALIDATE", "1")
+    _fill_outputs(b)
+    v.run("verify")
+    res = v.results()
+    for key in ("accepted_len", "next_token", "accepted_node"):
+        np.testing.assert_array_equal(res[key], ref[key])
+    np.testing.assert_array_equal(res["out"], ref["out"])
+
+
+@pytest.mark.parametrize("which", ["accept", "verify"])
+@pytest.mark.parametrize("bad", ["token_eq_vocab", "token_negative", "uniform_one", "q_zero_at_token"])
+def test_contract_violation_is_reported(gpu_lib, monkeypatch, which, bad):
+    print(f"[case] validation on, {bad} via spec_{which}", flush=True)
+    pool = _pool()
+    b = DeviceBatch(pool, "cuda")
+    v = Verifier(b)
+    # request 2 (k = 5): its second draft token, and the uniform of that node
+    q0 = int(pool.q_start[2])
+    t = q0 - 2 + 1                       # token of node 2 (offset n - 1 = 1)
+    if bad == "token_eq_vocab":
+        b.tokens[t] = pool.vocab
+    elif bad == "token_negative":
+        b.tokens[t] = -1
+    elif bad == "uniform_one":
+        b.uniforms[q0 + 2] = 1.0
+    else:
+        x = int(b.tokens[t].item())
+        b.probs[int(pool.d_start[2]) + 1, x] = 0.0     # node 2's parent is node 1 (chain)
+    monkeypatch.setenv("SPEC_DEBUG_VALIDATE", "1")
+    _fill_outputs(b)
+    with pytest.raises(B.SpecError) as e:
+        v.run(which)
+    assert e.value.status == B.SPEC_ERR_INVALID_ARG
+    _untouched(b, attn=(which == "verify"))
+
+
+def test_unset_or_zero_means_unchecked(gpu_lib, monkeypatch):
+    print("[case] validation off ('0')", flush=True)
+    pool = _pool()
+    b = DeviceBatch(pool, "cuda")
+    v = Verifier(b)
+    b.uniforms[int(pool.q_start[1])] = 1.0     # outside [0, 1): not checked, no read outside the arguments
+    monkeypatch.setenv("SPEC_DEBUG_VALIDATE", "0")
+    v.run("accept")
+    res = v.results()
+    assert (res["accepted_len"] >= 0).all() and (res["next_token"] >= 0).all()
