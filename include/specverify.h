@@ -228,6 +228,16 @@ SPEC_API const char* spec_status_str(spec_status_t status);
 /* SPEC_ABI_VERSION of the built library. */
 SPEC_API int32_t spec_abi_version(void);
 
+/* Diagnostics: the device's plain streaming read rate, reported beside the
+ * vendor HBM peak.  Reads `bytes` bytes at `src` (device memory, 16-byte
+ * aligned, `bytes` a multiple of 16) once, with coalesced 16-byte loads from
+ * `blocks` work-groups of 256 threads, and writes one word per work-group to
+ * `out` [blocks] (device memory; the words only keep the loads live).
+ * Enqueued on `stream`; the caller times it.  SPEC_ERR_INVALID_ARG for a
+ * null pointer, a misaligned `src` or size, or blocks outside [1, 65536]. */
+SPEC_API spec_status_t spec_stream_read_probe(const void* src, size_t bytes, uint32_t* out, int32_t blocks,
+                                              void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -18,7 +18,7 @@ SPEC_MAX_DRAFT = 16
 SPEC_MAX_TREE_NODES = 32
 
 EXPORTS = ("spec_workspace_bytes", "spec_verify_attn", "spec_accept", "spec_verify",
-           "spec_status_str", "spec_abi_version")
+           "spec_status_str", "spec_abi_version", "spec_stream_read_probe")
 
 
 class SpecRequests(C.Structure):
@@ -99,6 +99,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.spec_status_str.restype = C.c_char_p
     lib.spec_abi_version.argtypes = []
     lib.spec_abi_version.restype = C.c_int32
+    lib.spec_stream_read_probe.argtypes = [C.c_void_p, C.c_size_t, C.c_void_p, C.c_int32, C.c_void_p]
+    lib.spec_stream_read_probe.restype = C.c_int
     _lib = lib
     return lib
 
@@ -137,6 +139,10 @@ def spec_verify(req, attn, acc, ws: int, ws_bytes: int, staging: int, staging_by
 
 def spec_abi_version() -> int:
     return int(load().spec_abi_version())
+
+
+def spec_stream_read_probe(src, nbytes, out, blocks, stream):
+    return load().spec_stream_read_probe(src, nbytes, out, blocks, stream)
 
 
 def make_requests(ctx_len, draft_len=None, tree_parent=None):

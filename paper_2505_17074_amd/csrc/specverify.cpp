@@ -551,4 +551,12 @@ const char* spec_status_str(spec_status_t status) {
 
 int32_t spec_abi_version(void) { return SPEC_ABI_VERSION; }
 
+spec_status_t spec_stream_read_probe(const void* src, size_t bytes, uint32_t* out, int32_t blocks, void* stream) {
+  if (!src || !out || bytes == 0 || bytes % 16 || !aligned16(src) || blocks < 1 || blocks > 65536)
+    return SPEC_ERR_INVALID_ARG;
+  return sv::launch_stream_read(src, bytes, out, blocks, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? SPEC_OK
+             : SPEC_ERR_HIP;
+}
+
 }  // extern "C"

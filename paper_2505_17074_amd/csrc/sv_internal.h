@@ -119,5 +119,6 @@ hipError_t launch_accept(const AccParams& p, hipStream_t s);
 // and 4 (draft probability at a draft token not > 0).
 hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_t s);
 hipError_t launch_upload(const void* host_mapped, void* dst, size_t bytes, hipStream_t s);
+hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* out, int blocks, hipStream_t s);
 
 }  // namespace sv

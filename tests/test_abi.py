@@ -188,3 +188,14 @@ def test_workspace_grows_with_work(lib):
     b = _ws(_req(ctx=(100, 100, 100, 100), k=(2, 3, 4, 5)), _attn(), _acc())
     c = _ws(_req(), _attn(), _acc(vocab=128256, logits_stride=128256, probs_stride=128256))
     assert a[1] <= b[1] and _ws(_req(), _attn(), _acc())[1] < c[1]
+
+
+def test_stream_probe_rejects_bad_arguments(lib):
+    # every case fails its host check before any HIP call
+    assert B.spec_stream_read_probe(0, 1024, FAKE, 64, None) == B.SPEC_ERR_INVALID_ARG
+    assert B.spec_stream_read_probe(FAKE + 8, 1024, FAKE, 64, None) == B.SPEC_ERR_INVALID_ARG
+    assert B.spec_stream_read_probe(FAKE, 1000, FAKE, 64, None) == B.SPEC_ERR_INVALID_ARG
+    assert B.spec_stream_read_probe(FAKE, 0, FAKE, 64, None) == B.SPEC_ERR_INVALID_ARG
+    assert B.spec_stream_read_probe(FAKE, 1024, 0, 64, None) == B.SPEC_ERR_INVALID_ARG
+    assert B.spec_stream_read_probe(FAKE, 1024, FAKE, 0, None) == B.SPEC_ERR_INVALID_ARG
+    assert B.spec_stream_read_probe(FAKE, 1024, FAKE, 65537, None) == B.SPEC_ERR_INVALID_ARG

@@ -92,3 +92,20 @@ def test_unset_or_zero_means_unchecked(gpu_lib, monkeypatch):
     v.run("accept")
     res = v.results()
     assert (res["accepted_len"] >= 0).all() and (res["next_token"] >= 0).all()
+
+
+def test_stream_read_probe_reads_every_word(gpu_lib):
+    print("[case] stream read probe", flush=True)
+    n = (1 << 20) + 48                      # a ragged tail after the eight-load rounds
+    src = torch.zeros(n, dtype=torch.uint8, device="cuda")
+    src.view(torch.int32)[::7] = 0x5A5A5A5A
+    out = torch.empty(1 << 16, dtype=torch.int32, device="cuda")
+    for blocks in (1, 3, 64):
+        out.zero_()
+        B.check(B.spec_stream_read_probe(src.data_ptr(), n, out.data_ptr(), blocks,
+                                         torch.cuda.current_stream().cuda_stream), "probe")
+        torch.cuda.synchronize()
+        # the XOR of every word read, folded over the work-groups, equals the XOR of the buffer
+        got = np.bitwise_xor.reduce(out[:blocks].cpu().numpy().view(np.uint32))
+        want = np.bitwise_xor.reduce(src.cpu().numpy().view(np.uint32))
+        assert got == want, blocks
