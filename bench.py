@@ -176,7 +176,7 @@ def main():
     stream = torch.cuda.current_stream(dev)
 
     K, Wm = args.steps, args.warmup
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
     for e4 in ev:
         for e in e4:
             e.record(stream)          # materialise the events
@@ -227,8 +227,17 @@ def main():
         ver.acc.event_begin, ver.acc.event_end = ev[k][2].cuda_event, ev[k][3].cuda_event
         ver.run("accept", stream)
     torch.cuda.synchronize()
-    ver.acc.event_begin = ver.acc.event_end = None
     t_acc_us = float(np.mean([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)]) * 1e3)
+    # the row-statistics kernel alone, in a loop of its own (an event between
+    # the two acceptance kernels would lengthen the total above)
+    for k in range(K):
+        ver.run("attn", stream)
+        ver.acc.event_begin, ver.acc.event_end, ver.acc.event_mid = ev[k][2].cuda_event, None, ev[k][4].cuda_event
+        ver.run("accept", stream)
+    torch.cuda.synchronize()
+    ver.acc.event_begin = ver.acc.event_end = ver.acc.event_mid = None
+    t_rows_us = float(np.mean([ev[k][2].elapsed_time(ev[k][4]) for k in range(K)]) * 1e3)
+    logit_bytes = int(work["Nq"]) * pool.vocab * (2 if pool.logit_dtype == W.BF16 else 4)
     achieved = work["attn_bytes"] / (t_attn_us * 1e-6) / 1e9
     traffic = measured_traffic(args.workload)
     # tokens a step emits: the accepted drafts plus the final token, per request
@@ -264,7 +273,10 @@ def main():
         "accepted_plus_bonus_tokens_per_s": emitted / (ms * 1e-3),
         "accept": {"kernels_us": t_acc_us, "algorithmic_bytes_upper": work["accept_bytes"],
                    "achieved_GBs": work["accept_bytes"] / (t_acc_us * 1e-6) / 1e9,
-                   "frac": work["accept_bytes"] / (t_acc_us * 1e-6) / 1e9 / HBM_PEAK_GBS},
+                   "frac": work["accept_bytes"] / (t_acc_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                   # the streaming kernel alone (every target logit once): begin -> mid event
+                   "rowstats_us": t_rows_us, "rowstats_bytes": logit_bytes,
+                   "rowstats_frac": logit_bytes / (t_rows_us * 1e-6) / 1e9 / HBM_PEAK_GBS},
     }
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(pool, args.cpu_seconds)

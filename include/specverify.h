@@ -65,7 +65,7 @@ extern "C" {
 #define SPEC_API
 #endif
 
-#define SPEC_ABI_VERSION 1
+#define SPEC_ABI_VERSION 2
 #define SPEC_MAX_DRAFT 16        /* chain drafts per request */
 #define SPEC_MAX_TREE_NODES 32   /* token-tree nodes per request, root included */
 
@@ -179,10 +179,13 @@ typedef struct spec_accept_args {
   int32_t* accepted_len;
   int32_t* next_token;
   int32_t* accepted_node;
-  /* Optional profiling: hipEvent_t handles recorded on `stream` right before
-   * the first and right after the last acceptance kernel (NULL = none). */
+  /* Optional profiling: hipEvent_t handles recorded on the stream the
+   * acceptance kernels run on, right before the first, right after the last,
+   * and between the row-statistics kernel and the decision kernel
+   * (NULL = none). */
   void* event_begin;
   void* event_end;
+  void* event_mid;
 } spec_accept_args_t;
 
 /* Workspace sizes for a call with these arguments (either args pointer may

@@ -61,7 +61,8 @@ class SpecAcceptArgs(C.Structure):
                 ("next_token", C.c_void_p),
                 ("accepted_node", C.c_void_p),
                 ("event_begin", C.c_void_p),
-                ("event_end", C.c_void_p)]
+                ("event_end", C.c_void_p),
+                ("event_mid", C.c_void_p)]
 
 
 class SpecError(RuntimeError):

@@ -400,15 +400,15 @@ hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_
   return hipGetLastError();
 }
 
-hipError_t launch_accept(const AccParams& p, hipStream_t s) {
+hipError_t launch_accept(const AccParams& p, hipStream_t s, hipEvent_t mid) {
   dim3 block(kAccThreads);
-  if (p.bf16) {
-    acc_rowstats<uint16_t><<<dim3(p.Nq * p.nch), block, 0, s>>>(p);
-    acc_decide_select<uint16_t><<<dim3(p.B * p.nch), block, 0, s>>>(p);
-  } else {
-    acc_rowstats<float><<<dim3(p.Nq * p.nch), block, 0, s>>>(p);
-    acc_decide_select<float><<<dim3(p.B * p.nch), block, 0, s>>>(p);
-  }
+  if (p.bf16) acc_rowstats<uint16_t><<<dim3(p.Nq * p.nch), block, 0, s>>>(p);
+  else acc_rowstats<float><<<dim3(p.Nq * p.nch), block, 0, s>>>(p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (mid && (e = hipEventRecord(mid, s)) != hipSuccess) return e;
+  if (p.bf16) acc_decide_select<uint16_t><<<dim3(p.B * p.nch), block, 0, s>>>(p);
+  else acc_decide_select<float><<<dim3(p.B * p.nch), block, 0, s>>>(p);
   return hipGetLastError();
 }
 

@@ -469,7 +469,7 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
 
   auto launch_acc = [&](hipStream_t st) -> bool {
     if (acc->event_begin && hipEventRecord(static_cast<hipEvent_t>(acc->event_begin), st) != hipSuccess) return false;
-    if (sv::launch_accept(c, st) != hipSuccess) return false;
+    if (sv::launch_accept(c, st, static_cast<hipEvent_t>(acc->event_mid)) != hipSuccess) return false;
     if (acc->event_end && hipEventRecord(static_cast<hipEvent_t>(acc->event_end), st) != hipSuccess) return false;
     return true;
   };

@@ -199,3 +199,32 @@ def test_stream_probe_rejects_bad_arguments(lib):
     assert B.spec_stream_read_probe(FAKE, 1024, 0, 64, None) == B.SPEC_ERR_INVALID_ARG
     assert B.spec_stream_read_probe(FAKE, 1024, FAKE, 0, None) == B.SPEC_ERR_INVALID_ARG
     assert B.spec_stream_read_probe(FAKE, 1024, FAKE, 65537, None) == B.SPEC_ERR_INVALID_ARG
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    """The ctypes structures of the binding against the C header, field by
+    field (offsets and sizes from a program compiled with the system gcc)."""
+    import ctypes as C
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not found")
+    structs = {"spec_requests_t": B.SpecRequests, "spec_attn_args_t": B.SpecAttnArgs,
+               "spec_accept_args_t": B.SpecAcceptArgs}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{os.path.join(ROOT, "include", "specverify.h")}"',
+             "int main(void) {"]
+    for cname, cls in structs.items():
+        lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
+        for field, _ in cls._fields_:
+            lines.append(f'  printf("{cname} {field} %zu\\n", offsetof({cname}, {field}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c11", "-o", str(exe), str(src)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l.strip()}
+    for cname, cls in structs.items():
+        assert got[(cname, "size")] == C.sizeof(cls), cname
+        for field, _ in cls._fields_:
+            assert got[(cname, field)] == getattr(cls, field).offset, (cname, field)
