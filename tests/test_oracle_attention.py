@@ -214,3 +214,58 @@ def test_bf16_storage_widens_exactly():
     bits = np.array([[[0x3F80, 0xC000, 0x3F81, 0x0000]]], dtype=np.uint16)   # 1, -2, 1.0078125, 0
     out = verify_attention(bits[:, :, :4], bits, bits, [0], [1], 1, dtype="bf16")
     np.testing.assert_array_equal(out[0, 0], [1.0, -2.0, 1.0078125, 0.0])
+
+
+def _brute(q, k, v, ctx, n_q, Hkv, parent=None):
+    """The definition written out with Python loops and math.exp: for request
+    i, query head h, node j -- KV head h // G, the visible set (the cached
+    positions plus the ancestors-or-self of j, causal for a chain), scores
+    scaled by 1/sqrt(d), softmax with the max subtracted, the weighted sum of
+    the visible V rows."""
+    import math
+    Nq, Hq, d = q.shape
+    G = Hq // Hkv
+    out = np.zeros(q.shape, np.float64)
+    q0 = kv0 = 0
+    for c, n in zip(ctx, n_q):
+        for j in range(n):
+            if parent is None:
+                anc = set(range(j + 1))
+            else:
+                anc, a = set(), j
+                while a >= 0:
+                    anc.add(a)
+                    a = parent[a]
+            vis = list(range(c)) + [c + t for t in sorted(anc)]
+            for h in range(Hq):
+                g = h // G
+                s = []
+                for t in vis:
+                    acc = 0.0
+                    for e in range(d):
+                        acc += float(q[q0 + j, h, e]) * float(k[kv0 + t, g, e])
+                    s.append(acc / math.sqrt(d))
+                mx = max(s)
+                w = [math.exp(x - mx) for x in s]
+                tot = sum(w)
+                for e in range(d):
+                    out[q0 + j, h, e] = sum(wt * float(v[kv0 + t, g, e]) for wt, t in zip(w, vis)) / tot
+        q0 += n
+        kv0 += c + n
+    return out
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(2, 2), (4, 2)])
+def test_matches_brute_force_loops_chain(Hq, Hkv):
+    ctx, n_q = [0, 5, 8], [3, 1, 4]
+    q, k, v = _batch(ctx, n_q, Hq, Hkv, 8)
+    np.testing.assert_allclose(verify_attention(q, k, v, ctx, n_q, Hkv), _brute(q, k, v, ctx, n_q, Hkv),
+                               rtol=1e-12, atol=1e-12)
+
+
+def test_matches_brute_force_loops_tree():
+    parent = [-1, 0, 0, 1, 2]
+    ctx, n_q = [3, 0], [5, 5]
+    q, k, v = _batch(ctx, n_q, 4, 2, 6)
+    np.testing.assert_allclose(verify_attention(q, k, v, ctx, n_q, 2, tree_parent=parent),
+                               _brute(q, k, v, ctx, n_q, 2, parent=parent), rtol=1e-12, atol=1e-12)
