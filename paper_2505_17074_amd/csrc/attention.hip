@@ -20,10 +20,6 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
-  return __uint_as_float(static_cast<uint32_t>(b) << 16);
-}
-
 __device__ __forceinline__ float wave_max(float x) {
   for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
   return x;
@@ -490,10 +486,6 @@ template <typename T>
 __device__ __forceinline__ float load_elem(const T* p, int64_t i);
 template <>
 __device__ __forceinline__ float load_elem<float>(const float* p, int64_t i) { return p[i]; }
-template <>
-__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p, int64_t i) {
-  return bf16_to_f32(p[i]);
-}
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void attn_split_valu(AttnParams p) {

@@ -129,31 +129,71 @@ int device_cus() {
   return cus[dev];
 }
 
-// Work-groups of the bf16 split kernel one compute unit holds, by waves per
-// work-group (registers and LDS of the d = 128 build, as measured).
-int groups_per_cu(int waves) {
-  static const int table[6] = {0, 3, 3, 2, 2, 1};
-  return table[std::min(std::max(waves, 1), 5)];
+// Work-groups of the bf16 split kernel that run at once per compute unit.
+// Measured, not taken from the occupancy calculator (which allows 3 for the
+// 4- and 5-wave builds): with 64 equal streams cut into 8 pieces each (512
+// items on 256 compute units) every width, at d = 64 and d = 128, runs 7-27%
+// faster than with 9 pieces each (576 items), whose last 64 items form a
+// second, nearly empty round.
+int groups_per_cu(int /*waves*/) { return 2; }
+
+// Piece length for a stream of L >= 1 keys and a split of s >= 1 keys: the
+// stream cut into ceil(L / s) equal parts, rounded up to 32 keys (a short
+// trailing piece would leave its work-group idle most of the kernel while its
+// partial costs the same).  Every piece but the last has this length.
+int piece_len(int L, int64_t s) {
+  const int64_t n0 = (L + s - 1) / s;
+  return (int)(((L + n0 - 1) / n0 + 31) / 32 * 32);
+}
+// Pieces of that length covering the stream; non-increasing in s.
+int pieces_for(int L, int64_t s) {
+  const int piece = piece_len(L, s);
+  return (L + piece - 1) / piece;
 }
 
-// Keys per split piece.  `slots` = work-groups the device runs at once.
-// Pieces are at most kMaxPiece keys: a longer item, started first, still
-// outlasts the rest of the kernel once the other work-groups have drained
-// (measured on ragged batches: 6464-key pieces 28% slower than 4096).  With
-// fewer (request, KV head, head group) streams than slots, pieces shrink to
-// about one per slot.  They stay >= 40 * rows keys, so the fp32 partials
-// (rows x d x 4 bytes, written once and read once by the combine) remain a
-// few percent of the K/V bytes a piece streams (32 rows x d x 2 x 2 per 32
-// keys), and >= 256 keys.
+// Keys per split piece.  `slots` = work-groups the device runs at once;
+// `len[i]` = keys of request i, each the length of `mult[i]` streams (one per
+// KV head and head group).  Pieces stay >= 40 * rows keys, so the fp32
+// partials (rows x d x 4 bytes, written once and read once by the combine)
+// remain a few percent of the K/V bytes a piece streams (32 rows x d x 2 x 2
+// per 32 keys), and >= 256 keys.
+//  - At least as many streams as slots: pieces of at most kMaxPiece keys,
+//    dispatched longest first.  A longer item, started first, still outlasts
+//    the rest of the kernel once the other work-groups have drained (measured
+//    on ragged batches: 6464-key pieces 28% slower than 4096).
+//  - Fewer streams than slots: the smallest split whose items all fit one
+//    round of slots, so every work-group takes exactly one item and none waits
+//    for a second round (on 8 requests of 16K-32K keys x 8 KV heads, 504 items
+//    of <= 3264 keys: about 7% faster than 408 items of <= 4096 keys, and 24%
+//    faster than 528 items of <= 3072).
 constexpr int64_t kMaxPiece = 4096;
-int auto_split(int64_t key_streams, int64_t streams, int rows_max, int64_t slots) {
+constexpr int64_t kMaxSplit = 1 << 20;
+int auto_split(const std::vector<int>& len, const std::vector<int>& mult, int rows_max, int64_t slots) {
   slots = std::max<int64_t>(slots, 1);
-  int64_t s = kMaxPiece;
-  if (streams < slots) s = std::min<int64_t>(s, (key_streams + slots - 1) / slots);
-  s = std::max<int64_t>(s, 40 * (int64_t)rows_max);
-  s = std::max<int64_t>(s, 256);
-  s = (s + 31) / 32 * 32;
-  return (int)std::min<int64_t>(s, 1 << 20);
+  int64_t lo = std::max<int64_t>(40 * (int64_t)rows_max, 256);
+  lo = std::min<int64_t>((lo + 31) / 32 * 32, kMaxSplit);
+  int64_t streams = 0;
+  int max_len = 1;
+  for (size_t i = 0; i < len.size(); ++i) {
+    streams += mult[i];
+    max_len = std::max(max_len, len[i]);
+  }
+  if (streams >= slots) return (int)std::max(kMaxPiece, lo);
+  auto items = [&](int64_t s) {
+    int64_t n = 0;
+    for (size_t i = 0; i < len.size(); ++i) n += (int64_t)pieces_for(len[i], s) * mult[i];
+    return n;
+  };
+  // items() is non-increasing in s; items(hi) = streams < slots unless a
+  // request is longer than kMaxSplit keys
+  const int64_t hi = std::max(lo, std::min<int64_t>(((int64_t)max_len + 31) / 32 * 32, kMaxSplit));
+  if (items(lo) <= slots || items(hi) > slots) return (int)(items(lo) <= slots ? lo : hi);
+  int64_t a = lo / 32, b = hi / 32;        // items(32 a) > slots >= items(32 b)
+  while (b - a > 1) {
+    const int64_t m = (a + b) / 2;
+    if (items(32 * m) <= slots) b = m; else a = m;
+  }
+  return (int)(32 * b);
 }
 
 spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
@@ -231,8 +271,7 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
     const int Hq = attn->num_q_heads, Hkv = attn->num_kv_heads, G = Hq / Hkv;
     const int rmax = sv::max_rows_per_item(bf, D);
     // query-head groups per request so that heads * n_i <= rmax
-    std::vector<int> groups(P.B), hpg(P.B);
-    int64_t streams = 0, nstreams = 0;
+    std::vector<int> groups(P.B), hpg(P.B), len(P.B), mult(P.B);
     int rows_max = 1;
     for (int i = 0; i < P.B; ++i) {
       const int n = P.reqs[i].nq;
@@ -240,27 +279,23 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
       const int ng = (G + hmax - 1) / hmax;
       hpg[i] = (G + ng - 1) / ng;                      // balanced, still <= hmax
       groups[i] = (G + hpg[i] - 1) / hpg[i];
-      streams += ((int64_t)P.reqs[i].ctx + n) * Hkv * groups[i];
-      nstreams += (int64_t)Hkv * groups[i];
+      len[i] = P.reqs[i].ctx + n;
+      mult[i] = Hkv * groups[i];
       rows_max = std::max(rows_max, hpg[i] * n);
     }
     const int64_t slots = (int64_t)device_cus() * (bf ? groups_per_cu((rows_max + 15) / 16) : 2);
-    P.split = attn->split_kv > 0 ? attn->split_kv : auto_split(streams, nstreams, rows_max, slots);
+    P.split = attn->split_kv > 0 ? attn->split_kv : auto_split(len, mult, rows_max, slots);
     int64_t part = 0;
     int nr = 1;
     {
       int64_t n_items = 0;
-      for (int i = 0; i < P.B; ++i)
-        n_items += ((int64_t)P.reqs[i].ctx + P.reqs[i].nq + P.split - 1) / P.split * Hkv * groups[i];
+      for (int i = 0; i < P.B; ++i) n_items += (int64_t)pieces_for(len[i], P.split) * mult[i];
       P.items.reserve((size_t)n_items);
     }
     for (int i = 0; i < P.B; ++i) {
       ReqInfo& q = P.reqs[i];
-      const int L = q.ctx + q.nq;
-      // equal 32-aligned pieces: a short trailing piece would leave its
-      // work-group idle most of the kernel while its partial costs the same
-      q.nseg = (L + P.split - 1) / P.split;
-      const int piece = ((L + q.nseg - 1) / q.nseg + 31) / 32 * 32;
+      const int L = len[i];
+      const int piece = piece_len(L, P.split);
       q.nseg = (L + piece - 1) / piece;
       q.part0 = (int32_t)part;
       if (q.nseg > 1) part += (int64_t)q.nseg * q.nq * Hq;
