@@ -28,8 +28,8 @@ MFMA_BF16_PEAK = 2.5e15         # MI355X dense bf16 matrix FLOP/s, vendor figure
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="mha7b_b32")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -175,6 +175,12 @@ def main():
     ver = Verifier(batch)
     stream = torch.cuda.current_stream(dev)
 
+    # The device's stream ceilings first: about 90 GB of reads and copies
+    # (some 20 ms), which also bring the clocks to their loaded state before
+    # the warm-up steps (from a cold start the first milliseconds of steps run
+    # several percent slower).
+    read_ceiling, copy_rate = stream_ceilings_gbs(dev)
+
     K, Wm = args.steps, args.warmup
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
     for e4 in ev:
@@ -243,7 +249,6 @@ def main():
     # tokens a step emits: the accepted drafts plus the final token, per request
     # (the same inputs every step, so the last step's outputs stand for all)
     emitted = int(batch.accepted_len.to(torch.int64).sum().item()) + pool.batch
-    read_ceiling, copy_rate = stream_ceilings_gbs(dev)
 
     line = {
         "metric": METRIC,

@@ -400,16 +400,25 @@ hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_
   return hipGetLastError();
 }
 
-hipError_t launch_accept(const AccParams& p, hipStream_t s, hipEvent_t mid) {
+hipError_t launch_rowstats(const AccParams& p, hipStream_t s) {
   dim3 block(kAccThreads);
   if (p.bf16) acc_rowstats<uint16_t><<<dim3(p.Nq * p.nch), block, 0, s>>>(p);
   else acc_rowstats<float><<<dim3(p.Nq * p.nch), block, 0, s>>>(p);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (mid && (e = hipEventRecord(mid, s)) != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_decide(const AccParams& p, hipStream_t s) {
+  dim3 block(kAccThreads);
   if (p.bf16) acc_decide_select<uint16_t><<<dim3(p.B * p.nch), block, 0, s>>>(p);
   else acc_decide_select<float><<<dim3(p.B * p.nch), block, 0, s>>>(p);
   return hipGetLastError();
+}
+
+hipError_t launch_accept(const AccParams& p, hipStream_t s, hipEvent_t mid) {
+  hipError_t e = launch_rowstats(p, s);
+  if (e != hipSuccess) return e;
+  if (mid && (e = hipEventRecord(mid, s)) != hipSuccess) return e;
+  return launch_decide(p, s);
 }
 
 }  // namespace sv

@@ -115,6 +115,9 @@ hipError_t launch_attention(const AttnParams& p, int dtype_bf16, int nr_max, hip
 hipError_t launch_combine(const AttnParams& p, hipStream_t s);
 // Both acceptance kernels; `mid` (optional) is recorded between them.
 hipError_t launch_accept(const AccParams& p, hipStream_t s, hipEvent_t mid = nullptr);
+// the two halves of launch_accept: row statistics, then decision and sample
+hipError_t launch_rowstats(const AccParams& p, hipStream_t s);
+hipError_t launch_decide(const AccParams& p, hipStream_t s);
 // Debug check of the device-resident acceptance inputs: *flag (device) ends
 // as the OR of 1 (draft token id outside [0, V)), 2 (uniform outside [0, 1))
 // and 4 (draft probability at a draft token not > 0).
