@@ -67,6 +67,15 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 #ifndef SV_WPE_W34
 #define SV_WPE_W34 1
 #endif
+// Cache policy of the K/V tile transfers: the buffer instructions'
+// cachepolicy immediate, bit 1 = nt, the non-temporal (streaming) hint.  Every
+// K/V byte is read exactly once per call, and with the hint the tile stream
+// runs 10-14 % faster on every workload measured (a plain read kernel over
+// 2 GiB: 5.9 TB/s without, 6.6 TB/s with it); sc1 alone changes nothing.
+#ifndef SV_KV_CPOL
+#define SV_KV_CPOL 2
+#endif
+
 #ifndef SV_NS_W1
 #define SV_NS_W1 4
 #endif
@@ -177,7 +186,7 @@ __device__ __forceinline__ void issue_tile(char* stage, __amdgpu_buffer_rsrc_t r
       const bool isv = j >= G::IPM;
       const int jj = isv ? j - G::IPM : j;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(isv ? rv : rk, (lds_void_t*)(stage + (isv ? G::MAT : 0) + jj * 1024),
-                                               16, X.off[q], soff, 0, 0);
+                                               16, X.off[q], soff, 0, SV_KV_CPOL);
     }
   } else {
 #pragma unroll
@@ -190,7 +199,7 @@ __device__ __forceinline__ void issue_tile(char* stage, __amdgpu_buffer_rsrc_t r
       const uint32_t chunk_bytes = full - (uint32_t)row * (uint32_t)row_bytes;
       const int key = min(t0 + row, ke - 1);       // >= kb >= 0: items are never empty
       __builtin_amdgcn_raw_ptr_buffer_load_lds(isv ? rv : rk, (lds_void_t*)(stage + (isv ? G::MAT : 0) + jj * 1024),
-                                               16, (uint32_t)key * (uint32_t)row_bytes + chunk_bytes, 0u, 0, 0);
+                                               16, (uint32_t)key * (uint32_t)row_bytes + chunk_bytes, 0u, 0, SV_KV_CPOL);
     }
   }
 }
