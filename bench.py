@@ -175,12 +175,6 @@ def main():
     ver = Verifier(batch)
     stream = torch.cuda.current_stream(dev)
 
-    # The device's stream ceilings first: about 90 GB of reads and copies
-    # (some 20 ms), which also bring the clocks to their loaded state before
-    # the warm-up steps (from a cold start the first milliseconds of steps run
-    # several percent slower).
-    read_ceiling, copy_rate = stream_ceilings_gbs(dev)
-
     K, Wm = args.steps, args.warmup
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
     for e4 in ev:
@@ -249,6 +243,9 @@ def main():
     # tokens a step emits: the accepted drafts plus the final token, per request
     # (the same inputs every step, so the last step's outputs stand for all)
     emitted = int(batch.accepted_len.to(torch.int64).sum().item()) + pool.batch
+    # the device's stream ceilings last: their 20 ms of full-rate reads and
+    # copies leave the steps that follow them several percent slower
+    read_ceiling, copy_rate = stream_ceilings_gbs(dev)
 
     line = {
         "metric": METRIC,
