@@ -83,13 +83,20 @@ class DeviceBatch:
 class Verifier:
     """Runs spec_verify / spec_verify_attn / spec_accept on one DeviceBatch.
 
-    Owns the device workspace and a ring of pinned staging buffers; before a
-    staging slot is rewritten, the event recorded after its previous call is
-    polled until it completes (a spin, not a sleeping wait, so the host never
-    wakes late), so calls may be issued back to back without a device sync.
+    Owns the device workspace and a ring of `ring` pinned staging buffers,
+    one per call in turn.  The slots used since the last event are covered by
+    one event, recorded after every `event_every`-th call (and before a call
+    on a different stream): each event is a marker packet on the stream, and
+    one per call cost the steps 4-7 us.  Before a slot is rewritten, the
+    event covering its last use is polled until it completes (a spin, not a
+    sleeping wait, so the host never wakes late).  A slot's last use is
+    `ring` >= `event_every` calls back, so it is always covered by then.
+    Calls may be issued back to back without a device sync.
     """
 
-    def __init__(self, batch: DeviceBatch, split_kv: int = 0, ring: int = 8):
+    def __init__(self, batch: DeviceBatch, split_kv: int = 0, ring: int = 32, event_every: int = 8):
+        if event_every < 1 or ring < event_every:
+            raise ValueError("need ring >= event_every >= 1")
         self.batch = batch
         self.req = batch.requests()
         self.attn = batch.attn_args(split_kv)
@@ -101,38 +108,57 @@ class Verifier:
         self.ws_ptr = (self._ws.data_ptr() + 255) // 256 * 256
         self.staging_bytes = host
         self._staging = [torch.empty(max(host, 1), dtype=torch.uint8, pin_memory=True) for _ in range(ring)]
-        self._events = [torch.cuda.Event() for _ in range(ring)]
-        self._used = [False] * ring
-        self._i = 0
+        self._every = event_every
+        self._slot_ev = [None] * ring      # the event covering each slot's last use
+        self._pending = []                 # slots used since the last event
+        self._pending_stream = None
+        self._i = 0                        # calls issued
 
-    def _slot(self):
+    def _cover(self):
+        # a new event each time: one recorded again later, perhaps on another
+        # stream, would no longer order the slots that still hold it
+        if self._pending:
+            ev = torch.cuda.Event()
+            ev.record(self._pending_stream)
+            for s in self._pending:
+                self._slot_ev[s] = ev
+            self._pending = []
+
+    def _slot(self, stream):
+        if self._pending and stream != self._pending_stream:
+            self._cover()
         s = self._i % len(self._staging)
-        self._i += 1
-        if self._used[s]:
-            ev = self._events[s]
+        ev = self._slot_ev[s]              # never pending: fewer than event_every <= ring calls are
+        if ev is not None:
             while not ev.query():
                 pass
+        self._i += 1
         return s
 
     def _done(self, s, stream):
-        self._events[s].record(stream)
-        self._used[s] = True
+        self._slot_ev[s] = None
+        self._pending.append(s)
+        self._pending_stream = stream
+        if len(self._pending) >= self._every:
+            self._cover()
 
     def run(self, which: str = "verify", stream: Optional[torch.cuda.Stream] = None) -> None:
         stream = stream or torch.cuda.current_stream(self.batch.device)
-        s = self._slot()
+        s = self._slot(stream)
         stg = self._staging[s].data_ptr()
         h = stream.cuda_stream
-        if which == "verify":
-            st = B.spec_verify(self.req, self.attn, self.acc, self.ws_ptr, self.ws_bytes, stg, self.staging_bytes, h)
-        elif which == "attn":
-            st = B.spec_verify_attn(self.req, self.attn, self.ws_ptr, self.ws_bytes, stg, self.staging_bytes, h)
-        elif which == "accept":
-            st = B.spec_accept(self.req, self.acc, self.ws_ptr, self.ws_bytes, stg, self.staging_bytes, h)
-        else:
-            raise ValueError(which)
+        try:
+            if which == "verify":
+                st = B.spec_verify(self.req, self.attn, self.acc, self.ws_ptr, self.ws_bytes, stg, self.staging_bytes, h)
+            elif which == "attn":
+                st = B.spec_verify_attn(self.req, self.attn, self.ws_ptr, self.ws_bytes, stg, self.staging_bytes, h)
+            elif which == "accept":
+                st = B.spec_accept(self.req, self.acc, self.ws_ptr, self.ws_bytes, stg, self.staging_bytes, h)
+            else:
+                raise ValueError(which)
+        finally:
+            self._done(s, stream)       # a failed call's slot is covered like any other
         B.check(st, f"spec_{which}")
-        self._done(s, stream)
 
     def results(self) -> dict:
         torch.cuda.synchronize(self.batch.device)
