@@ -19,6 +19,13 @@ What it computes (each function cites the passage it follows):
   distribution on rejection (Sec. 2.2), and the one extra LLM token when every
   candidate is accepted (Sec. 4.3, the "+1" of Eq. (6)).
 
+* ``scheduler.simulate`` -- the LAPS-SD request scheduler of Algorithm 1
+  (Sec. 4: priority queues with exponential thresholds, demotion by attained
+  service, the acceptance-rate stability test, the Eq. (6) estimate, and
+  perceptible-SJF / non-perceptible-FCFS inside a queue) and the FCFS, LAS
+  and predicted-length SJF baselines, round by round on integer microsecond
+  times.
+
 Everything is computed in float64 from the stored input values (bf16 and fp32
 widen to fp64 exactly).  Both parts are exact results with a plain definition,
 so the oracle is that definition written out, not an approximation.
