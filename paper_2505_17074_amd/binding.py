@@ -18,7 +18,13 @@ SPEC_MAX_DRAFT = 16
 SPEC_MAX_TREE_NODES = 32
 
 EXPORTS = ("spec_workspace_bytes", "spec_verify_attn", "spec_accept", "spec_verify",
-           "spec_status_str", "spec_abi_version", "spec_stream_read_probe")
+           "spec_status_str", "spec_abi_version", "spec_stream_read_probe",
+           "spec_sched_create", "spec_sched_destroy", "spec_sched_submit", "spec_sched_next",
+           "spec_sched_report", "spec_sched_query", "spec_sched_simulate")
+
+SPEC_SCHED_FCFS, SPEC_SCHED_LP_SJF, SPEC_SCHED_SJF_EXACT, SPEC_SCHED_LAS, SPEC_SCHED_LAPS_SD = range(5)
+SCHED_POLICY = {"fcfs": SPEC_SCHED_FCFS, "lp_sjf": SPEC_SCHED_LP_SJF, "sjf_exact": SPEC_SCHED_SJF_EXACT,
+                "las": SPEC_SCHED_LAS, "laps_sd": SPEC_SCHED_LAPS_SD}
 
 
 class SpecRequests(C.Structure):
@@ -65,6 +71,53 @@ class SpecAcceptArgs(C.Structure):
                 ("event_mid", C.c_void_p)]
 
 
+class SpecSchedParams(C.Structure):
+    _fields_ = [("K", C.c_int32),
+                ("M", C.c_int32),
+                ("S1_up_us", C.c_int64),
+                ("gamma", C.c_int32),
+                ("pad0", C.c_int32),
+                ("delta", C.c_double),
+                ("t_ssm_us", C.c_int64),
+                ("t_llm_us", C.c_int64),
+                ("swap_us_per_token", C.c_int64)]
+
+
+class SpecSchedState(C.Structure):
+    _fields_ = [("attained_us", C.c_int64),
+                ("queue", C.c_int32),
+                ("perceptible", C.c_int32),
+                ("finished", C.c_int32),
+                ("rounds", C.c_int32),
+                ("A", C.c_double),
+                ("T_est_us", C.c_double)]
+
+
+class SpecSchedRequest(C.Structure):
+    _fields_ = [("arrival_us", C.c_int64),
+                ("round_us", C.c_int64),
+                ("prompt_tokens", C.c_int32),
+                ("out_len", C.c_int32),
+                ("pred_len", C.c_int32),
+                ("draft", C.c_int32),
+                ("accepted", C.POINTER(C.c_int32)),
+                ("n_accepted", C.c_int32),
+                ("pad0", C.c_int32)]
+
+
+class SpecSchedResult(C.Structure):
+    _fields_ = [("completion_us", C.POINTER(C.c_int64)),
+                ("round_req", C.POINTER(C.c_int32)),
+                ("round_start_us", C.POINTER(C.c_int64)),
+                ("max_rounds", C.c_int64),
+                ("n_rounds", C.c_int64),
+                ("switches", C.c_int64),
+                ("switch_us", C.c_int64),
+                ("perceptible", C.POINTER(C.c_int32)),
+                ("A", C.POINTER(C.c_double)),
+                ("T_est_us", C.POINTER(C.c_double))]
+
+
 class SpecError(RuntimeError):
     def __init__(self, status: int, where: str, text: str):
         super().__init__(f"{where}: {text} (status {status})")
@@ -102,6 +155,22 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.spec_abi_version.restype = C.c_int32
     lib.spec_stream_read_probe.argtypes = [C.c_void_p, C.c_size_t, C.c_void_p, C.c_int32, C.c_void_p]
     lib.spec_stream_read_probe.restype = C.c_int
+    lib.spec_sched_create.argtypes = [C.c_int32, P(SpecSchedParams), C.c_int32, P(C.c_void_p)]
+    lib.spec_sched_create.restype = C.c_int
+    lib.spec_sched_destroy.argtypes = [C.c_void_p]
+    lib.spec_sched_destroy.restype = None
+    lib.spec_sched_submit.argtypes = [C.c_void_p, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int64,
+                                      P(C.c_int32)]
+    lib.spec_sched_submit.restype = C.c_int
+    lib.spec_sched_next.argtypes = [C.c_void_p, C.c_int64, P(C.c_int32)]
+    lib.spec_sched_next.restype = C.c_int
+    lib.spec_sched_report.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_int64, C.c_int32]
+    lib.spec_sched_report.restype = C.c_int
+    lib.spec_sched_query.argtypes = [C.c_void_p, C.c_int32, P(SpecSchedState)]
+    lib.spec_sched_query.restype = C.c_int
+    lib.spec_sched_simulate.argtypes = [P(SpecSchedRequest), C.c_int32, C.c_int32, P(SpecSchedParams),
+                                        P(SpecSchedResult)]
+    lib.spec_sched_simulate.restype = C.c_int
     _lib = lib
     return lib
 

@@ -22,8 +22,12 @@ def lib():
 
 
 def _declared():
-    text = open(HEADER).read()
-    return re.findall(r"SPEC_API\s+[\w\s\*]+?\b(spec_\w+)\s*\(", text)
+    names = []
+    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if h.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", h)).read()
+            names += re.findall(r"SPEC_API\s+[\w\s\*]+?\b(spec_\w+)\s*\(", text)
+    return names
 
 
 def test_exports_every_declared_symbol(lib):
@@ -210,8 +214,10 @@ def test_struct_layouts_match_the_header(tmp_path):
     if shutil.which("gcc") is None:
         pytest.skip("gcc not found")
     structs = {"spec_requests_t": B.SpecRequests, "spec_attn_args_t": B.SpecAttnArgs,
-               "spec_accept_args_t": B.SpecAcceptArgs}
-    lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{os.path.join(ROOT, "include", "specverify.h")}"',
+               "spec_accept_args_t": B.SpecAcceptArgs, "spec_sched_params_t": B.SpecSchedParams,
+               "spec_sched_state_t": B.SpecSchedState, "spec_sched_request_t": B.SpecSchedRequest,
+               "spec_sched_result_t": B.SpecSchedResult}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{os.path.join(ROOT, "include", "specsched.h")}"',
              "int main(void) {"]
     for cname, cls in structs.items():
         lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
