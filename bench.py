@@ -110,6 +110,63 @@ def pct(xs, q):
     return float(np.percentile(np.asarray(xs, dtype=np.float64), q))
 
 
+def scheduler_closed_loop(dev, seed: int) -> dict:
+    """The LAPS-SD scheduler driven by the verify step's own accepted counts:
+    50 requests' per-round accepted counts from the library's acceptance
+    kernels (one batched spec_accept per round index), then every policy on
+    the one-request-at-a-time server model, and the native scheduler's cost
+    per decision."""
+    from paper_2505_17074_amd import closed_loop as CL
+    from paper_2505_17074_amd.scheduler import simulate
+    cfg = CL.LoopConfig()
+    wl = CL.make_workload(cfg, seed)
+    t0 = time.perf_counter()
+    traces = CL.gpu_traces(cfg, wl, seed, device=dev)
+    t_traces = time.perf_counter() - t0
+    reqs = CL.requests_from(cfg, wl, traces)
+    params = CL.default_params(cfg)
+    res = CL.evaluate(reqs, params)
+    lat = {pol: r["avg_latency_ms"] for pol, r in res.items()}
+    sweep = {K: simulate(reqs, "laps_sd", CL.default_params(cfg, K=K), log=False)["avg_latency"] / 1000.0
+             for K in (1, 2, 3, 4, 6, 8, 10)}
+    reps, t0 = 20, time.perf_counter()
+    for _ in range(reps):
+        o = simulate(reqs, "laps_sd", params, log=False)
+    dec_us = (time.perf_counter() - t0) / reps / o["n_rounds"] * 1e6
+    return {"workload": f"{cfg.requests} requests, draft {cfg.draft}, output lengths log-normal (median "
+                        f"{cfg.out_median}), predicted with log-normal error sigma {cfg.pred_sigma}, per-request "
+                        f"acceptance from target noise sigma in {list(cfg.sigma)}; rounds "
+                        f"{cfg.draft} x {cfg.t_ssm_us} + {cfg.t_llm_us} us; KV swap {cfg.swap_us_per_token} us/token",
+            "rounds_traced": int(traces.shape[1]), "trace_s": t_traces,
+            "mean_tokens_per_round": float((traces + 1).mean()),
+            "avg_latency_ms": lat,
+            "laps_sd_vs": {pol: lat[pol] / lat["laps_sd"] for pol in ("fcfs", "lp_sjf", "las", "sjf_exact")},
+            "switches": {pol: r["switches"] for pol, r in res.items()},
+            "laps_sd_perceptible": res["laps_sd"]["perceptible"],
+            "laps_sd_avg_latency_ms_by_K": sweep,
+            "native_decision_us": dec_us}
+
+
+def scheduler_oracle_decision_us(dev, seed: int) -> float:
+    """The scheduler oracle's cost per decision on the same workload, with
+    host-drawn traces of the same shape (the cost does not depend on the
+    accepted counts' source)."""
+    from oracle.scheduler import Params, Request, simulate
+    from paper_2505_17074_amd import closed_loop as CL
+    import numpy as np
+    cfg = CL.LoopConfig()
+    wl = CL.make_workload(cfg, seed)
+    rng = np.random.default_rng(seed)
+    traces = rng.binomial(cfg.draft, rng.uniform(0.2, 0.8, size=(cfg.requests, 1)),
+                          size=(cfg.requests, int(wl.out_len.max())))
+    reqs = [Request(r.arrival, r.prompt, r.out_len, r.pred_len, r.draft, r.round_us, list(r.accepted))
+            for r in CL.requests_from(cfg, wl, traces)]
+    p = CL.default_params(cfg)
+    t0 = time.perf_counter()
+    o = simulate(reqs, "laps_sd", Params(p.K, p.S1_up, p.M, p.gamma, p.delta, p.t_ssm, p.t_llm, p.swap_us_per_token))
+    return (time.perf_counter() - t0) / len(o["log"]) * 1e6
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -337,8 +394,10 @@ def main():
                    "rowstats_us": t_rows_us, "rowstats_bytes": logit_bytes,
                    "rowstats_frac": logit_bytes / (t_rows_us * 1e-6) / 1e9 / HBM_PEAK_GBS},
     }
+    line["scheduler"] = scheduler_closed_loop(dev, args.seed)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(pool, args.cpu_seconds)
+        line["cpu_baseline"]["scheduler_oracle_decision_us"] = scheduler_oracle_decision_us(dev, args.seed)
     print(json.dumps(line), flush=True)
 
 

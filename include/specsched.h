@@ -21,12 +21,15 @@
  *   SPEC_SCHED_LAS        least attained service first, re-decided after
  *                         every round (Sec. 3, the LAS baseline of Sec. 5.1).
  *   SPEC_SCHED_LAPS_SD    Algorithm 1:
- *     - K priority queues; queue j (0-based) holds requests whose attained
- *       service E (the sum of their round times: speculation plus
- *       verification, Sec. 4.2) lies in [S_down(j), S_up(j)), with
- *       S_up(j) = S1_up_us * M^j for j < K-1, the last queue unbounded, and
- *       S_down(j) = S_up(j-1), S_down(0) = 0.  New requests enter queue 0;
- *       after every round a request moves to the queue its E falls in.
+ *     - K priority queues; queue j (0-based) covers service times in
+ *       [S_down(j), S_up(j)), with S_up(j) = S1_up_us * M^j for j < K-1,
+ *       the last queue unbounded, and S_down(j) = S_up(j-1), S_down(0) = 0.
+ *       New requests enter queue 0.  After every round a non-perceptible
+ *       request moves to the queue holding its attained service E (the sum
+ *       of its round times: speculation plus verification, Sec. 4.2); a
+ *       perceptible one to the queue holding max(E, T), T its Eq. (6)
+ *       estimate truncated to an integer ("moved to the corresponding
+ *       queue", Sec. 4.1).
  *     - The highest-priority non-empty queue is served (Sec. 4.2).  Inside
  *       it, perceptible requests go first, smallest Eq. (6) estimate first;
  *       then non-perceptible requests, earliest arrival first (Sec. 4.3).

@@ -33,11 +33,15 @@ Policies (`policy`):
   "las"        least attained service first, re-decided after every round
                (Sec. 3, Sec. 5.1 baseline).
   "laps_sd"    Algorithm 1 (Sec. 4.1-4.3):
-      - K queues; queue j (0-based here) holds requests whose attained
-        service E satisfies S_down(j) <= E < S_up(j), with
-        S_up(j) = S1_up * M^j for j < K-1, the last queue unbounded, and
-        S_down(j) = S_up(j-1), S_down(0) = 0.  New requests enter queue 0;
-        after every round the request moves to the queue its E falls in.
+      - K queues; queue j (0-based here) covers service times S with
+        S_down(j) <= S < S_up(j), where S_up(j) = S1_up * M^j for j < K-1,
+        the last queue is unbounded, S_down(j) = S_up(j-1) and
+        S_down(0) = 0.  New requests enter queue 0.  After every round a
+        non-perceptible request moves to the queue holding its attained
+        service E (Sec. 4.2); a perceptible one to the queue holding
+        max(E, T), its Eq. (6) estimate T ("moved to the corresponding
+        queue", Sec. 4.1), so that attained service takes over only if it
+        overruns its estimate.
       - The highest non-empty queue is served (inter-queue, Sec. 4.2).
       - Within it, perceptible requests go first, shortest estimated
         execution time first (SJF); then non-perceptible ones, earliest
@@ -56,11 +60,13 @@ Policies (`policy`):
 
 Readings of points the paper leaves open:
   * M is an integer >= 2, so every threshold is an exact integer.
-  * Perceptible requests keep being placed by attained service (the
-    demotion rule of Sec. 4.2 applies to every request), and "no preemption"
-    holds inside a queue only: were a perceptible request never preempted at
-    all, it would run to completion from the round it became perceptible,
-    and the SJF order among perceptible requests could never act.
+  * A perceptible request is placed by max(E, T) (above): its estimate
+    puts it in the queue it is expected to finish in, which is why, in the
+    paper's words, perceptible requests seldom exceed their queue's
+    threshold.  "No preemption" holds inside a queue only: were a
+    perceptible request never preempted at all, it would run to completion
+    from the round it became perceptible, and the SJF order among
+    perceptible requests could never act.
   * The SJF key is the Eq. (6) estimate itself (the paper's "request size"),
     not a remaining-time estimate; ties go to the earlier arrival, then the
     smaller index.
@@ -72,7 +78,8 @@ Floating point appears only in the rates, the stability test and Eq. (6).
 The operations and their order are fixed by the formulas above:
   * rate = accepted / drafted;
   * A = (left-to-right sum of the window) / gamma;
-  * T = float(n*Lp*T_SSM + Lp*T_LLM) / (float(n) * A + 1.0).
+  * T = float(n*Lp*T_SSM + Lp*T_LLM) / (float(n) * A + 1.0);
+  * the queue of a perceptible request uses T truncated to an integer.
 """
 from __future__ import annotations
 
@@ -209,7 +216,6 @@ def simulate(reqs: List[Request], policy: str, p: Optional[Params] = None) -> di
             completion[i] = now
             continue
         if policy == "laps_sd":
-            queue[i] = queue_of(E[i], p)
             if not perceptible[i] and r.draft > 0:
                 acc_sum[i] += a
                 drafted[i] += r.draft
@@ -223,6 +229,7 @@ def simulate(reqs: List[Request], policy: str, p: Optional[Params] = None) -> di
                             s += x
                         A[i] = s / p.gamma
                         T_est[i] = eq6_estimate(r.draft, r.pred_len, A[i], p.t_ssm, p.t_llm)
+            queue[i] = queue_of(max(E[i], int(T_est[i])) if perceptible[i] else E[i], p)
     latency = [completion[i] - reqs[i].arrival for i in range(N)]
     return {"completion": completion, "latency": latency,
             "avg_latency": sum(latency) / N if N else 0.0,

@@ -161,7 +161,6 @@ struct spec_sched {
       return;
     }
     if (policy == SPEC_SCHED_LAPS_SD) {
-      r.queue = queue_of(r.attained);
       if (!r.perceptible && r.draft > 0) {
         r.acc_sum += a;
         r.drafted += r.draft;
@@ -186,6 +185,9 @@ struct spec_sched {
           }
         }
       }
+      // a perceptible request goes to the queue of max(E, T): its estimate
+      // places it, attained service takes over if it overruns
+      r.queue = queue_of(r.perceptible ? std::max(r.attained, (int64_t)r.T) : r.attained);
     }
     place(id);
   }

@@ -180,17 +180,32 @@ def test_perceptible_first_then_fcfs_by_hand():
 def test_sjf_among_perceptible_by_hand():
     """D1 (predicted 10 tokens) and D2 (predicted 1000) both draft 4 and accept
     1 per round (rate 1/4, stable after one round): Eq. (6) with T_SSM = 1,
-    T_LLM = 10 gives 70 and 7000.  D1 runs 0-30 and drops to queue 1, D2 runs
-    30-60, drops, and keeps the server for 60-70 (queue 1 is then the top);
-    E arrives at 65 into queue 0 and runs 70-80.  At 80 the shorter estimate,
-    D1, goes first: its 27 remaining rounds end at 350, then D2's 26 at 610."""
+    T_LLM = 10 gives 70 and 7000, both beyond queue 0's 25 us, so each moves
+    to queue 1 as soon as it is perceptible.  D1 runs 0-10, D2 10-20 and then
+    keeps the server (queue 1 is the top, and a running perceptible request
+    is not preempted inside its queue) until E, arriving at 65 into queue 0,
+    takes 70-80.  At 80 the shorter estimate, D1, goes first: its 29
+    remaining rounds end at 370, then D2's 24 at 610."""
     D1 = Request(0, 0, 60, 10, 4, 10, [1] * 60)
     D2 = Request(0, 0, 60, 1000, 4, 10, [1] * 60)
     E = Request(65, 0, 1, 1, 0, 10, [0])
     out = simulate([D1, D2, E], "laps_sd", Params(K=2, S1_up=25, M=100, gamma=1, delta=1.0, t_ssm=1, t_llm=10))
     assert out["T_est"][:2] == [70.0, 7000.0]
-    assert [e[0] for e in out["log"]] == [0] * 3 + [1] * 4 + [2] + [0] * 27 + [1] * 26
-    assert out["completion"] == [350, 610, 80]
+    assert [e[0] for e in out["log"]] == [0] + [1] * 6 + [2] + [0] * 29 + [1] * 24
+    assert out["completion"] == [370, 610, 80]
+
+
+def test_estimate_places_a_perceptible_request():
+    """Queue 0 holds service below 100 us, queue 1 below 400.  A drafts 4,
+    accepts 2 per round (rate 1/2, stable after 2 rounds with gamma = 2):
+    with T_LLM = 10 and predicted length 100, T = 100*10 / 3 = 333.3, so after
+    its second round A sits in queue 1 although it has attained only 20 us,
+    and B (arriving at 5, queue 0) runs next."""
+    A = Request(0, 0, 30, 100, 4, 10, [2] * 30)
+    B = Request(5, 0, 2, 2, 0, 10, [0, 0])
+    out = simulate([A, B], "laps_sd", Params(K=3, S1_up=100, M=4, gamma=2, delta=0.01, t_llm=10))
+    assert out["T_est"][0] == pytest.approx(1000 / 3, rel=1e-15)
+    assert [e[0] for e in out["log"][:4]] == [0, 0, 1, 1]
 
 
 @pytest.mark.parametrize("policy", ["fcfs", "lp_sjf", "sjf_exact", "las", "laps_sd"])
