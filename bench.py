@@ -118,7 +118,8 @@ def scheduler_closed_loop(dev, seed: int) -> dict:
     per decision."""
     from paper_2505_17074_amd import closed_loop as CL
     from paper_2505_17074_amd.scheduler import simulate
-    cfg = CL.LoopConfig()
+    swap = CL.measure_swap(dev)
+    cfg = CL.LoopConfig(swap_us_per_token=swap["us_per_token"])
     wl = CL.make_workload(cfg, seed)
     t0 = time.perf_counter()
     traces = CL.gpu_traces(cfg, wl, seed, device=dev)
@@ -144,7 +145,10 @@ def scheduler_closed_loop(dev, seed: int) -> dict:
             "switches": {pol: r["switches"] for pol, r in res.items()},
             "laps_sd_perceptible": res["laps_sd"]["perceptible"],
             "laps_sd_avg_latency_ms_by_K": sweep,
-            "native_decision_us": dec_us}
+            "native_decision_us": dec_us,
+            "kv_swap": {"d2h_GBs": swap["d2h_GBs"], "h2d_GBs": swap["h2d_GBs"],
+                        "us_per_token_measured": swap["us_per_token"],
+                        "bytes_per_token": CL.KV_BYTES_PER_TOKEN}}
 
 
 def scheduler_oracle_decision_us(dev, seed: int) -> float:

@@ -17,8 +17,9 @@ Times (integer microseconds):
     (the per-token verification time Fig. 1 assumes for LLaMA-7B) and
     T_SSM = 0.5 ms per drafted token;
   * switching swaps a request's KV cache at `swap_us_per_token` per cached
-    token each way: 8 us (LLaMA-7B fp16 KV, 512 KB per token, over a
-    64 GB/s host link).
+    token each way.  The default of 8 us assumes LLaMA-7B fp16 KV (512 KB
+    per token) over a 64 GB/s host link; `measure_swap` times the copies on
+    the machine at hand, and the benchmark uses its figure.
 """
 from __future__ import annotations
 
@@ -58,6 +59,39 @@ class LoopWorkload:
     out_len: np.ndarray
     pred_len: np.ndarray
     sigma: np.ndarray
+
+
+KV_BYTES_PER_TOKEN = 2 * 32 * 4096 * 2     # LLaMA-7B: K and V, 32 layers, 4096 wide, fp16
+
+
+def measure_swap(device="cuda", tokens=(16, 64, 256, 1024, 4096), reps: int = 5) -> dict:
+    """KV swap cost on this machine (the switching cost of Sec. 3, Fig. 3):
+    device -> pinned host and host -> device copies of a request's KV cache
+    (KV_BYTES_PER_TOKEN per token), timed by events on the current stream.
+    Returns GB/s per direction and size, and the cost per cached token at the
+    largest size (both directions averaged), rounded up to whole us."""
+    import torch
+    top = max(tokens) * KV_BYTES_PER_TOKEN
+    dev = torch.empty(top, dtype=torch.uint8, device=device)
+    host = torch.empty(top, dtype=torch.uint8, pin_memory=True)
+    dev.fill_(1)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = {"d2h_GBs": {}, "h2d_GBs": {}}
+    for t in tokens:
+        nb = t * KV_BYTES_PER_TOKEN
+        for name, dst, src in (("d2h_GBs", host, dev), ("h2d_GBs", dev, host)):
+            dst[:nb].copy_(src[:nb], non_blocking=True)
+            e0.record()
+            for _ in range(reps):
+                dst[:nb].copy_(src[:nb], non_blocking=True)
+            e1.record()
+            torch.cuda.synchronize()
+            out[name][t] = nb * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    t = max(tokens)
+    gbs = 2.0 / (1.0 / out["d2h_GBs"][t] + 1.0 / out["h2d_GBs"][t])
+    out["us_per_token"] = int(np.ceil(KV_BYTES_PER_TOKEN / (gbs * 1e9) * 1e6))
+    del dev, host
+    return out
 
 
 def make_workload(cfg: LoopConfig, seed: int) -> LoopWorkload:
