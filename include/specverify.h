@@ -65,7 +65,7 @@ extern "C" {
 #define SPEC_API
 #endif
 
-#define SPEC_ABI_VERSION 2
+#define SPEC_ABI_VERSION 3
 #define SPEC_MAX_DRAFT 16        /* chain drafts per request */
 #define SPEC_MAX_TREE_NODES 32   /* token-tree nodes per request, root included */
 
@@ -121,6 +121,22 @@ typedef struct spec_requests {
  *   KV positions per split (a positive multiple of 32) -- results agree
  *   across splits within fp32 rounding.  Requests split more than once are
  *   merged by a second (combine) kernel.
+ *
+ * Paged KV cache (block_table != NULL; the PagedAttention layout the paper
+ * cites as serving practice, Sec. 6.2): k and v are page pools
+ * [num_pages, page_tokens, Hkv, d], kv_stride_tok / kv_stride_head their
+ * strides inside a page (a page spans page_tokens * kv_stride_tok elements).
+ * block_table (device, int32) holds request i's page ids at
+ * block_table[i * block_stride + j] for its logical pages
+ * j = 0 .. ceil((c_i + n_i) / page_tokens) - 1: logical KV row t of request
+ * i is row t % page_tokens of page block_table[i * block_stride +
+ * t / page_tokens], its verify rows last as in the packed layout.
+ * page_tokens is a positive multiple of 32; block_stride must hold every
+ * request's pages; bf16 only (SPEC_ERR_UNSUPPORTED for f32).  Page ids in
+ * [0, num_pages) are the caller's contract: an id outside is clamped into
+ * the pool, so nothing outside it is read, but its rows are meaningless.
+ * With the same rows the paged and packed layouts give bit-identical
+ * outputs.
  */
 typedef struct spec_attn_args {
   int32_t num_q_heads;
@@ -141,6 +157,12 @@ typedef struct spec_attn_args {
    * and right after the split-KV attention kernel (NULL = not recorded). */
   void* event_begin;
   void* event_end;
+  /* Paged KV cache (above); block_table NULL = the packed layout. */
+  const int32_t* block_table;
+  int32_t block_stride;
+  int32_t page_tokens;
+  int32_t num_pages;
+  int32_t pad0;
 } spec_attn_args_t;
 
 /*

@@ -98,3 +98,16 @@ def verify_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
         q0 += n
         kv0 += L
     return out
+
+
+def gather_paged(pool_rows: np.ndarray, block_table: np.ndarray, page_tokens: int, ctx_len, n_q) -> np.ndarray:
+    """The packed [Nkv, Hkv, d] rows of a paged cache (the PagedAttention
+    layout the paper cites as serving practice, Sec. 6.2): logical KV row t of
+    request i is row t % page_tokens of page block_table[i, t // page_tokens]
+    of the pool, given here as [num_pages * page_tokens, Hkv, d]."""
+    out = []
+    for i in range(len(ctx_len)):
+        for t in range(int(ctx_len[i]) + int(n_q[i])):
+            page = int(block_table[i, t // page_tokens])
+            out.append(pool_rows[page * page_tokens + t % page_tokens])
+    return np.stack(out)

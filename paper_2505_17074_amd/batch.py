@@ -94,12 +94,13 @@ class Verifier:
     Calls may be issued back to back without a device sync.
     """
 
-    def __init__(self, batch: DeviceBatch, split_kv: int = 0, ring: int = 32, event_every: int = 8):
+    def __init__(self, batch: DeviceBatch, split_kv: int = 0, ring: int = 32, event_every: int = 8,
+                 attn: Optional[B.SpecAttnArgs] = None):
         if event_every < 1 or ring < event_every:
             raise ValueError("need ring >= event_every >= 1")
         self.batch = batch
         self.req = batch.requests()
-        self.attn = batch.attn_args(split_kv)
+        self.attn = attn if attn is not None else batch.attn_args(split_kv)
         self.acc = batch.accept_args()
         st, dev, host = B.spec_workspace_bytes(self.req, self.attn, self.acc)
         B.check(st, "spec_workspace_bytes")
@@ -167,3 +168,49 @@ class Verifier:
                 "accepted_len": b.accepted_len.cpu().numpy(),
                 "next_token": b.next_token.cpu().numpy(),
                 "accepted_node": b.accepted_node.cpu().numpy()}
+
+
+class PagedKV:
+    """A DeviceBatch's K/V rows in page pools [num_pages, page_tokens, Hkv, d]
+    (the paged layout of specverify.h), pages in a seeded random order with
+    `spare` unused pages in between, and the block table [B, block_stride].
+    Rows past a request's length in its last page are zero.  `attn_args`
+    returns attention arguments that read the pools through the table."""
+
+    def __init__(self, batch: DeviceBatch, page_tokens: int = 64, seed: int = 0, spare: int = 3):
+        pool = batch.pool
+        P = int(page_tokens)
+        L = (pool.ctx_len.astype(np.int64) + pool.n_q.astype(np.int64))
+        pages = (L + P - 1) // P
+        total = int(pages.sum())
+        self.page_tokens, self.num_pages = P, total + int(spare)
+        self.block_stride = int(pages.max())
+        rng = np.random.default_rng(seed)
+        order = rng.permutation(self.num_pages)[:total].astype(np.int32)
+        table = np.zeros((pool.batch, self.block_stride), np.int32)
+        start = np.concatenate([[0], np.cumsum(pages)])
+        src, dst = [], []
+        kv0 = np.concatenate([[0], np.cumsum(L)])
+        for i in range(pool.batch):
+            table[i, :pages[i]] = order[start[i]:start[i + 1]]
+            t = np.arange(L[i])
+            src.append(kv0[i] + t)
+            dst.append(table[i, t // P].astype(np.int64) * P + t % P)
+        src = torch.from_numpy(np.concatenate(src)).to(batch.device)
+        dst = torch.from_numpy(np.concatenate(dst)).to(batch.device)
+        Hkv, d = batch.k.shape[1], batch.k.shape[2]
+        self.k = torch.zeros((self.num_pages * P, Hkv, d), dtype=batch.k.dtype, device=batch.device)
+        self.v = torch.zeros_like(self.k)
+        self.k[dst] = batch.k[src]
+        self.v[dst] = batch.v[src]
+        self.table = torch.from_numpy(table).to(batch.device)
+        self.table_np = table
+        self.batch = batch
+
+    def attn_args(self, split_kv: int = 0, scale: float = 0.0) -> B.SpecAttnArgs:
+        a = self.batch.attn_args(split_kv, scale)
+        a.k, a.v = self.k.data_ptr(), self.v.data_ptr()
+        a.kv_stride_tok, a.kv_stride_head = self.k.stride(0), self.k.stride(1)
+        a.block_table = self.table.data_ptr()
+        a.block_stride, a.page_tokens, a.num_pages = self.block_stride, self.page_tokens, self.num_pages
+        return a

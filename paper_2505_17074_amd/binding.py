@@ -51,7 +51,12 @@ class SpecAttnArgs(C.Structure):
                 ("out", C.c_void_p),
                 ("split_kv", C.c_int32),
                 ("event_begin", C.c_void_p),
-                ("event_end", C.c_void_p)]
+                ("event_end", C.c_void_p),
+                ("block_table", C.c_void_p),
+                ("block_stride", C.c_int32),
+                ("page_tokens", C.c_int32),
+                ("num_pages", C.c_int32),
+                ("pad0", C.c_int32)]
 
 
 class SpecAcceptArgs(C.Structure):

@@ -341,9 +341,15 @@ struct WavesPerEu {
   static constexpr int value = W == 5 ? 4 : (W >= 3 ? SV_WPE_W34 : 1);
 };
 
-template <int D, int W, int NS>
+// PG: paged KV cache.  A tile (32 keys, 32-aligned) never straddles a page
+// (pages hold a multiple of 32 tokens), so each tile's transfers take a buffer
+// resource based at its page, built from the block table entry (a
+// wave-uniform load, clamped into the pool, issued one ring step ahead of its
+// use); everything else is the packed path's code.
+template <int D, int W, int NS, bool PG>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(WavesPerEu<W>::value)))
 void attn_split_mfma(AttnParams p) {
+#if defined(__HIP_DEVICE_COMPILE__)   // the host pass needs the signature only
   using G = Geo<D>;
   constexpr int ET = D / 16, KS = D / 32;
   constexpr int PER = Xfer<D, W>::PER;
@@ -387,6 +393,34 @@ void attn_split_mfma(AttnParams p) {
     X.off[q] = xfer_offset<D>((w + q * W) % Xfer<D, W>::NI, lane, row_bytes, &row);
   }
 
+  // paged: this KV head's slice of page 0 of each pool, the item's block
+  // table row, and tile t's page id (tiles past the item's end re-read its
+  // last tile, as in the packed path)
+  const char* Kh = static_cast<const char*>(p.k) + (int64_t)it.kvh * p.kv_sh * 2;
+  const char* Vh = static_cast<const char*>(p.v) + (int64_t)it.kvh * p.kv_sh * 2;
+  const int32_t* btr = PG ? p.bt + (int64_t)it.req * p.bt_stride : nullptr;
+  const int last_t0 = it.kb + 32 * (ntiles - 1);
+  // (generic lambdas: instantiated only in the device pass, like the ring loop's)
+  auto page_of = [&](auto t) -> int {
+    const int t0 = min(it.kb + 32 * t, last_t0);
+    const int pg = btr[t0 / p.page_tokens];
+    return __builtin_amdgcn_readfirstlane(min(max(pg, 0), p.num_pages - 1));
+  };
+  auto issue = [&](char* stage, auto t, int pg) {
+    if constexpr (PG) {
+      const int t0 = min(it.kb + 32 * t, last_t0);
+      const int base = t0 - t0 % p.page_tokens;          // the page's first logical key
+      const int64_t pb = (int64_t)pg * p.page_bytes;
+      const int prange = p.page_tokens * row_bytes;
+      const __amdgpu_buffer_rsrc_t pk = __builtin_amdgcn_make_buffer_rsrc((void*)(Kh + pb), 0, prange, 0x00020000);
+      const __amdgpu_buffer_rsrc_t pv = __builtin_amdgcn_make_buffer_rsrc((void*)(Vh + pb), 0, prange, 0x00020000);
+      issue_tile<D, W>(stage, pk, pv, row_bytes, t0 - base, it.ke - base, w, lane, X);
+    } else {
+      (void)pg;
+      issue_tile<D, W>(stage, rk, rv, row_bytes, it.kb + 32 * t, it.ke, w, lane, X);
+    }
+  };
+
   {
     const int r = w * 16 + c16;
     const int j = (r < R) ? r % n : -1;
@@ -421,8 +455,7 @@ void attn_split_mfma(AttnParams p) {
   // alone, and hand the registers through an empty asm so that no later use
   // inherits a wait on the ring.
 #pragma unroll
-  for (int st = 0; st < NS - 1; ++st)
-    issue_tile<D, W>(lds + st * G::STAGE, rk, rv, row_bytes, it.kb + 32 * st, it.ke, w, lane, X);
+  for (int st = 0; st < NS - 1; ++st) issue(lds + st * G::STAGE, st, PG ? page_of(st) : 0);
   wait_vm<PER * (NS - 1)>();
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(S.q[ks]));
@@ -436,14 +469,15 @@ void attn_split_mfma(AttnParams p) {
         stop = true;
         return;
       }
+      // paged: the page of the tile issued below, loaded before the waits
+      // (the barrier's lgkmcnt wait covers it)
+      const int pg_next = (PG && t + NS - 1 < ntiles) ? page_of(t + NS - 1) : 0;
       // this wave's transfers of tile t have landed: NS-2 later tiles may still
       // be in flight, none in the item's last NS-2 tiles (over-waiting there)
       if (t + NS - 2 < ntiles) wait_vm<PER * (NS - 2)>();
       else wait_vm<0>();
       ring_barrier();                 // everyone's have landed; stage (t-1) % NS is free
-      if (t + NS - 1 < ntiles)
-        issue_tile<D, W>(lds + ((st + NS - 1) % NS) * G::STAGE, rk, rv, row_bytes, it.kb + 32 * (t + NS - 1), it.ke,
-                         w, lane, X);
+      if (t + NS - 1 < ntiles) issue(lds + ((st + NS - 1) % NS) * G::STAGE, t + NS - 1, pg_next);
       if (active) compute_tile<D, st * G::STAGE>(lds, S, it.kb + 32 * t, it.ke, ctx, p.scale_log2, lane);
     });
   }
@@ -483,6 +517,7 @@ void attn_split_mfma(AttnParams p) {
     const float4 v = *reinterpret_cast<const float4*>(ost + rl * (D + 4) + e4);
     *reinterpret_cast<float4*>((it.seg < 0 ? p.out : p.part_o) + o * D + e4) = v;
   }
+#endif
 }
 
 // ---------------------------------------------------------------------------
@@ -660,15 +695,15 @@ __global__ __launch_bounds__(256) void attn_combine(AttnParams p) {
   for (int x = 0; x < PER; ++x) p.out[((int64_t)qrow * p.Hq + h) * D + lane + 64 * x] = acc[x] * inv;
 }
 
-template <int D>
+template <int D, bool PG>
 hipError_t launch_mfma(const AttnParams& p, int nr, hipStream_t s) {
   const dim3 grid(p.n_items);
   switch (nr) {
-    case 1: attn_split_mfma<D, 1, SV_NS_W1><<<grid, dim3(64), 0, s>>>(p); break;
-    case 2: attn_split_mfma<D, 2, SV_NS_W2><<<grid, dim3(128), 0, s>>>(p); break;
-    case 3: attn_split_mfma<D, 3, SV_NS_W3><<<grid, dim3(192), 0, s>>>(p); break;
-    case 4: attn_split_mfma<D, 4, SV_NS_W4><<<grid, dim3(256), 0, s>>>(p); break;
-    case 5: attn_split_mfma<D, 5, SV_NS_W5><<<grid, dim3(320), 0, s>>>(p); break;
+    case 1: attn_split_mfma<D, 1, SV_NS_W1, PG><<<grid, dim3(64), 0, s>>>(p); break;
+    case 2: attn_split_mfma<D, 2, SV_NS_W2, PG><<<grid, dim3(128), 0, s>>>(p); break;
+    case 3: attn_split_mfma<D, 3, SV_NS_W3, PG><<<grid, dim3(192), 0, s>>>(p); break;
+    case 4: attn_split_mfma<D, 4, SV_NS_W4, PG><<<grid, dim3(256), 0, s>>>(p); break;
+    case 5: attn_split_mfma<D, 5, SV_NS_W5, PG><<<grid, dim3(320), 0, s>>>(p); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -695,8 +730,10 @@ int max_rows_per_item(int dtype_bf16, int D) { return dtype_bf16 ? 80 : 4096 / D
 hipError_t launch_attention(const AttnParams& p, int dtype_bf16, int nr_max, hipStream_t s) {
   hipError_t e = hipSuccess;
   if (p.n_items > 0) {
-    if (dtype_bf16) {
-      e = (p.D == 64) ? launch_mfma<64>(p, nr_max, s) : launch_mfma<128>(p, nr_max, s);
+    if (dtype_bf16 && p.bt) {
+      e = (p.D == 64) ? launch_mfma<64, true>(p, nr_max, s) : launch_mfma<128, true>(p, nr_max, s);
+    } else if (dtype_bf16) {
+      e = (p.D == 64) ? launch_mfma<64, false>(p, nr_max, s) : launch_mfma<128, false>(p, nr_max, s);
     } else {
       dim3 grid(p.n_items), block(256);
       if (p.D == 64) attn_split_valu<float, 64><<<grid, block, 0, s>>>(p);

@@ -86,6 +86,16 @@ spec_status_t check_attn(const spec_attn_args_t* a) {
   if (a->q_stride_tok % vec || a->q_stride_head % vec || a->kv_stride_tok % vec || a->kv_stride_head % vec)
     return SPEC_ERR_INVALID_ARG;
   if (a->split_kv < 0 || (a->split_kv > 0 && a->split_kv % 32)) return SPEC_ERR_INVALID_ARG;
+  if (a->block_table) {
+    // paged pools [num_pages, page_tokens, Hkv, d]: a token row holds every head
+    if (a->page_tokens < 32 || a->page_tokens % 32 || a->num_pages < 1 || a->block_stride < 1)
+      return SPEC_ERR_INVALID_ARG;
+    if (reinterpret_cast<uintptr_t>(a->block_table) % 4) return SPEC_ERR_INVALID_ARG;
+    if (a->kv_stride_head * (a->num_kv_heads - 1) + a->head_dim > a->kv_stride_tok) return SPEC_ERR_INVALID_ARG;
+    if (a->dtype != SPEC_BF16) return SPEC_ERR_UNSUPPORTED;
+    // one page's rows of one head are addressed with 32-bit offsets
+    if ((int64_t)a->page_tokens * a->kv_stride_tok * 2 >= INT32_MAX) return SPEC_ERR_UNSUPPORTED;
+  }
   return SPEC_OK;
 }
 
@@ -260,11 +270,17 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   }
 
   if (attn) {
-    // the bf16 kernels address one request's rows of one KV head with 32-bit offsets
     const int64_t elem = attn->dtype == SPEC_F32 ? 4 : 2;
-    for (int i = 0; i < P.B; ++i)
-      if (((int64_t)P.reqs[i].ctx + P.reqs[i].nq) * attn->kv_stride_tok * elem >= INT32_MAX)
+    for (int i = 0; i < P.B; ++i) {
+      const int64_t L = (int64_t)P.reqs[i].ctx + P.reqs[i].nq;
+      if (attn->block_table) {
+        // every logical page of the request has a block table entry
+        if ((L + attn->page_tokens - 1) / attn->page_tokens > attn->block_stride) return SPEC_ERR_INVALID_ARG;
+      } else if (L * attn->kv_stride_tok * elem >= INT32_MAX) {
+        // the packed path addresses one request's rows of one KV head with 32-bit offsets
         return SPEC_ERR_UNSUPPORTED;
+      }
+    }
     P.has_attn = true;
     const int bf = attn->dtype == SPEC_BF16;
     const int D = attn->head_dim;
@@ -464,6 +480,11 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     a.D = attn->head_dim;
     a.n_items = (int32_t)P.items.size();
     a.Nq = (int32_t)P.Nq;
+    a.bt = attn->block_table;
+    a.bt_stride = attn->block_stride;
+    a.page_tokens = attn->page_tokens;
+    a.num_pages = attn->num_pages;
+    a.page_bytes = (int64_t)attn->page_tokens * attn->kv_stride_tok * 2;
     std::memcpy(a.anc, P.topo.anc, sizeof(a.anc));
   }
   sv::AccParams c{};

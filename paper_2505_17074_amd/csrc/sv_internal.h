@@ -67,6 +67,13 @@ struct AttnParams {
   int32_t Hq, Hkv, G, D;
   int32_t n_items;
   int32_t Nq;
+  // paged KV cache (bt != nullptr): page pools, the block table and its row
+  // stride, tokens per page (a multiple of 32), pages in the pool, page bytes
+  const int32_t* bt;
+  int32_t bt_stride;
+  int32_t page_tokens;
+  int32_t num_pages;
+  int64_t page_bytes;
   uint32_t anc[kMaxNodes];   // ancestors-or-self masks (kernel arguments: uniform loads)
 };
 

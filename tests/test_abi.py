@@ -234,3 +234,28 @@ def test_struct_layouts_match_the_header(tmp_path):
         assert got[(cname, "size")] == C.sizeof(cls), cname
         for field, _ in cls._fields_:
             assert got[(cname, field)] == getattr(cls, field).offset, (cname, field)
+
+
+PAGED = dict(block_table=FAKE, block_stride=1, page_tokens=32, num_pages=10)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(), B.SPEC_OK),                                              # requests of 7 and 12 rows: one page each
+    (dict(page_tokens=0), B.SPEC_ERR_INVALID_ARG),
+    (dict(page_tokens=16), B.SPEC_ERR_INVALID_ARG),
+    (dict(page_tokens=48), B.SPEC_ERR_INVALID_ARG),
+    (dict(num_pages=0), B.SPEC_ERR_INVALID_ARG),
+    (dict(block_stride=0), B.SPEC_ERR_INVALID_ARG),
+    (dict(block_table=FAKE + 2), B.SPEC_ERR_INVALID_ARG),
+    (dict(kv_stride_tok=128), B.SPEC_ERR_INVALID_ARG),                # a token row must hold every head
+    (dict(dtype=B.SPEC_F32), B.SPEC_ERR_UNSUPPORTED),
+    (dict(page_tokens=1 << 23), B.SPEC_ERR_UNSUPPORTED),              # a page beyond 32-bit offsets
+])
+def test_paged_attention_checks(lib, kw, expect):
+    assert _ws(_req(), _attn(**{**PAGED, **kw}), None)[0] == expect
+
+
+def test_paged_block_stride_must_hold_every_page(lib):
+    # 3000 + 3 rows need 94 pages of 32
+    assert _ws(_req(ctx=(3000, 5), k=(2, 1)), _attn(**{**PAGED, "block_stride": 93}), None)[0] == B.SPEC_ERR_INVALID_ARG
+    assert _ws(_req(ctx=(3000, 5), k=(2, 1)), _attn(**{**PAGED, "block_stride": 94}), None)[0] == B.SPEC_OK

@@ -269,3 +269,28 @@ def test_matches_brute_force_loops_tree():
     q, k, v = _batch(ctx, n_q, 4, 2, 6)
     np.testing.assert_allclose(verify_attention(q, k, v, ctx, n_q, 2, tree_parent=parent),
                                _brute(q, k, v, ctx, n_q, 2, parent=parent), rtol=1e-12, atol=1e-12)
+
+
+def test_paged_gather_round_trip():
+    """Scatter packed rows into pages in a random order, gather them back
+    through the block table: the packed rows, exactly (and a page order that
+    differs only in its spare pages gathers the same)."""
+    from oracle.attention import gather_paged
+    rng = np.random.default_rng(3)
+    ctx, nq, P = [5, 70, 0, 33], [3, 1, 5, 4], 32
+    L = [c + n for c, n in zip(ctx, nq)]
+    rows = rng.standard_normal((sum(L), 2, 8))
+    pages = [(x + P - 1) // P for x in L]
+    num_pages = sum(pages) + 4
+    order = rng.permutation(num_pages)
+    table = np.zeros((len(L), max(pages)), np.int64)
+    pool = np.full((num_pages * P, 2, 8), np.nan)
+    k, start = 0, 0
+    for i, x in enumerate(L):
+        for j in range(pages[i]):
+            table[i, j] = order[k]
+            k += 1
+        for t in range(x):
+            pool[table[i, t // P] * P + t % P] = rows[start + t]
+        start += x
+    np.testing.assert_array_equal(gather_paged(pool, table, P, ctx, nq), rows)
