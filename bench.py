@@ -303,6 +303,28 @@ def main():
     t_alone_us = float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]) * 1e3)
     t_call_us = float(np.mean([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)]) * 1e3)
 
+    # The same attention alone and the same steps over a paged KV cache:
+    # 64-token pages in a seeded random order, read through the block table.
+    from paper_2505_17074_amd.batch import PagedKV
+    pk = PagedKV(batch, 64, seed=args.seed)
+    pver = Verifier(batch, attn=pk.attn_args())
+    for _ in range(Wm):
+        pver.run("verify", stream)
+    torch.cuda.synchronize()
+    for k in range(K):
+        pver.attn.event_begin, pver.attn.event_end = ev[k][0].cuda_event, ev[k][1].cuda_event
+        pver.run("attn", stream)
+    torch.cuda.synchronize()
+    pver.attn.event_begin = pver.attn.event_end = None
+    t_paged_us = float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]) * 1e3)
+    t0 = time.perf_counter()
+    for k in range(K):
+        pver.run("verify", stream)
+    torch.cuda.synchronize()
+    ms_paged = (time.perf_counter() - t0) * 1e3 / K
+    del pver, pk
+    torch.cuda.empty_cache()
+
     # Cold steps: the same step after a flush of the caches, each timed by
     # events around the call on the caller's stream.  Back to back, every step
     # re-reads the same target logits, which the K/V stream (non-temporal
@@ -381,6 +403,10 @@ def main():
                      "frac_alone": work["attn_bytes"] / (t_alone_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
                      # the whole spec_verify_attn call alone: plan upload + split + combine
                      "call_us_alone": t_call_us,
+                     # the same kernel over a paged KV cache (64-token pages, random order)
+                     "paged": {"page_tokens": 64, "kernel_us_alone": t_paged_us,
+                               "frac_alone": work["attn_bytes"] / (t_paged_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                               "ms_per_step": ms_paged},
                      "frac_call_alone": work["attn_bytes"] / (t_call_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
                      "mfma_util": work["attn_flops"] / (t_attn_us * 1e-6) / MFMA_BF16_PEAK,
                      "stream_read_GBs": read_ceiling, "frac_of_stream_read": achieved / read_ceiling,

@@ -398,12 +398,18 @@ void attn_split_mfma(AttnParams p) {
   // last tile, as in the packed path)
   const char* Kh = static_cast<const char*>(p.k) + (int64_t)it.kvh * p.kv_sh * 2;
   const char* Vh = static_cast<const char*>(p.v) + (int64_t)it.kvh * p.kv_sh * 2;
-  const int32_t* btr = PG ? p.bt + (int64_t)it.req * p.bt_stride : nullptr;
+  // The block table is read through the constant address space with a
+  // wave-uniform index, so the page ids come in by scalar loads: a vector
+  // load would count among the ring's outstanding transfers, and its
+  // consumer's wait would drain the whole ring every tile.
+  typedef __attribute__((address_space(4))) const int32_t cint32_t;
+  const cint32_t* btr = PG ? (const cint32_t*)(p.bt + (int64_t)it.req * p.bt_stride) : nullptr;
   const int last_t0 = it.kb + 32 * (ntiles - 1);
   // (generic lambdas: instantiated only in the device pass, like the ring loop's)
   auto page_of = [&](auto t) -> int {
     const int t0 = min(it.kb + 32 * t, last_t0);
-    const int pg = btr[t0 / p.page_tokens];
+    const int idx = __builtin_amdgcn_readfirstlane(t0 / p.page_tokens);
+    const int pg = btr[idx];
     return __builtin_amdgcn_readfirstlane(min(max(pg, 0), p.num_pages - 1));
   };
   auto issue = [&](char* stage, auto t, int pg) {
