@@ -33,6 +33,8 @@ def parse():
     ap.add_argument("--workload", default="mha7b_b32")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-sched", action="store_true",
+                    help="skip the scheduler's closed loop (thousands of small launches; for profiler runs)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only copy BYTES device-to-device three times (the calibration run for the "
@@ -424,10 +426,12 @@ def main():
                    "rowstats_us": t_rows_us, "rowstats_bytes": logit_bytes,
                    "rowstats_frac": logit_bytes / (t_rows_us * 1e-6) / 1e9 / HBM_PEAK_GBS},
     }
-    line["scheduler"] = scheduler_closed_loop(dev, args.seed)
+    if not args.no_sched:
+        line["scheduler"] = scheduler_closed_loop(dev, args.seed)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(pool, args.cpu_seconds)
-        line["cpu_baseline"]["scheduler_oracle_decision_us"] = scheduler_oracle_decision_us(dev, args.seed)
+        if not args.no_sched:
+            line["cpu_baseline"]["scheduler_oracle_decision_us"] = scheduler_oracle_decision_us(dev, args.seed)
     print(json.dumps(line), flush=True)
 
 
