@@ -31,5 +31,5 @@ widen to fp64 exactly).  Both parts are exact results with a plain definition,
 so the oracle is that definition written out, not an approximation.
 """
 from .attention import verify_attention, ancestors_or_self, widen  # noqa: F401
-from .accept import (accept_chain, accept_tree, verify_accept, softmax64,  # noqa: F401
+from .accept import (accept_chain, accept_tree, accept_tree_sequential, verify_accept, softmax64,  # noqa: F401
                      inverse_cdf, NEAR_TIE, NEAR_TIE_MASS)

@@ -122,6 +122,44 @@ def tree_depths(parent: Sequence[int]) -> np.ndarray:
     return depth
 
 
+def accept_tree_sequential(p_rows: np.ndarray, q_rows: dict, tokens: Sequence[int],
+                           uniforms: Sequence[float], parent: Sequence[int]) -> dict:
+    """One request of sequential sibling verification over a token tree, the
+    multi-step speculative sampling of SpecInfer (the token-tree system the
+    paper's evaluation follows, Sec. 5.1).  Starting at the root, the current
+    node's children -- drafted i.i.d. from its draft row q -- are tested in
+    BFS order against a running target distribution p' (first the node's own
+    target row): child c is accepted iff u_c * q(x_c) < p'(x_c); a rejection
+    replaces p' by max(0, p' - q) normalised (kept as it is if that has zero
+    mass, reachable only through rounding).  The first accepted child becomes
+    the current node; when no child is accepted, or the node is a leaf, the
+    final token is drawn from p' with the last uniform.  Arguments as for
+    accept_tree."""
+    n = len(parent)
+    depth = tree_depths(parent)
+    children = {u: [c for c in range(1, n) if int(parent[c]) == u] for u in range(n)}
+    node, margins = 0, []
+    while True:
+        pp = np.asarray(p_rows[node], dtype=np.float64)
+        nxt_node = None
+        for c in children[node]:
+            q = q_rows[node]
+            x = int(tokens[c - 1])
+            ok, m = _test(float(uniforms[c - 1]), pp[x], q[x])
+            margins.append(m)
+            if ok:
+                nxt_node = c
+                break
+            w = np.maximum(0.0, pp - q)
+            if w.sum() > 0.0:
+                pp = w / w.sum()
+        if nxt_node is None:
+            break
+        node = nxt_node
+    nxt, m_s = inverse_cdf(pp, float(uniforms[n - 1]))
+    return _result(int(depth[node]), nxt, node, margins, m_s)
+
+
 def accept_tree(p_rows: np.ndarray, q_rows: dict, tokens: Sequence[int],
                 uniforms: Sequence[float], parent: Sequence[int]) -> dict:
     """One request of the tree rule.  p_rows [n, V]; q_rows maps each node that
@@ -158,7 +196,8 @@ def verify_accept(target_logits: np.ndarray, draft_probs: np.ndarray,
                   draft_tokens: np.ndarray, uniforms: np.ndarray,
                   n_q: Sequence[int], dtype: str = "f32",
                   tree_parent: Optional[Sequence[int]] = None,
-                  requests: Optional[Sequence[int]] = None) -> dict:
+                  requests: Optional[Sequence[int]] = None,
+                  tree_rule: str = "independent") -> dict:
     """Acceptance for a packed batch (layouts as in the C interface).
 
     Request i owns target rows q0_i .. q0_i + n_i - 1 (q0 = running sum of
@@ -192,7 +231,8 @@ def verify_accept(target_logits: np.ndarray, draft_probs: np.ndarray,
             r = accept_chain(p_rows, q_rows, toks, us)
         else:
             q_rows = {node: widen(draft_probs[d0[i] + rnk], dtype) for rnk, node in enumerate(has_child)}
-            r = accept_tree(p_rows, q_rows, toks, us, tree_parent)
+            rule = accept_tree_sequential if tree_rule == "sequential" else accept_tree
+            r = rule(p_rows, q_rows, toks, us, tree_parent)
         for key in keys:
             res[key][i] = r[key]
         res["near_tie"][i] = r["near_tie"]

@@ -259,3 +259,85 @@ def test_tree_deepest_node_smallest_index():
     toks2 = [int(np.argmin(P[0] / Q[0])), 1, 2, 3, 4, 5]
     r = accept_tree(P, Q, toks2, [1 - 2 ** -24] + [0.0] * 5 + [0.5], parent)
     assert (r["accepted_node"], r["accepted_len"]) == (5, 2)
+
+
+def _sibling_first_token(p0, q0, child_rows, m):
+    """Distribution of the first emitted token of a one-level tree with m
+    children drafted i.i.d. from q0, by enumerating the child tokens and the
+    cells of every uniform (cut where a decision can change)."""
+    from oracle import accept_tree_sequential
+    V = len(p0)
+    parent = [-1] + [0] * m
+    p_rows = np.stack([p0] + child_rows)
+    # the running distributions after 0..m rejections do not depend on the tokens
+    runs = [p0]
+    for _ in range(m):
+        w = np.maximum(0.0, runs[-1] - q0)
+        runs.append(w / w.sum() if w.sum() > 0 else runs[-1])
+    dist = np.zeros(V)
+    for xs in itertools.product(range(V), repeat=m):
+        wq = np.prod([q0[x] for x in xs])
+        if wq == 0:
+            continue
+        test_cells = [_cells([min(1.0, runs[i][x] / q0[x])]) for i, x in enumerate(xs)]
+        for combo in itertools.product(*test_cells):
+            us = [c[0] for c in combo]
+            lw = np.prod([c[1] for c in combo])
+            for uf, lf in _cells(_cdf_breaks(runs[m])):
+                r = accept_tree_sequential(p_rows, {0: q0}, list(xs), us + [uf], parent)
+                y = list(xs)[r["accepted_node"] - 1] if r["accepted_len"] == 1 else r["next_token"]
+                dist[y] += wq * lw * lf
+    return dist
+
+
+@pytest.mark.parametrize("m", [2, 3])
+@pytest.mark.parametrize("case", range(4))
+def test_sequential_siblings_preserve_the_target(m, case):
+    """SpecInfer's guarantee: with children drafted i.i.d. from q, sequential
+    sibling verification emits a first token distributed exactly as p."""
+    V = 8
+    rng = np.random.default_rng(50 + case)
+    if case == 0:
+        p0, q0 = _dist(V, rng), _dist(V, rng)
+    elif case == 1:                                   # p = q: the first child is always accepted
+        p0 = _dist(V, rng)
+        q0 = p0.copy()
+    elif case == 2:                                   # disjoint supports: every child rejected
+        p0 = np.r_[_dist(4, rng), np.zeros(4)]
+        q0 = np.r_[np.zeros(4), _dist(4, rng)]
+    else:                                             # one-hot draft
+        p0, q0 = _dist(V, rng), np.eye(V)[3]
+    child_rows = [_dist(V, rng) for _ in range(m)]
+    np.testing.assert_allclose(_sibling_first_token(p0, q0, child_rows, m), p0, rtol=0, atol=1e-12)
+
+
+def test_sequential_on_a_path_is_the_chain_rule():
+    """Every node with one child: sequential sibling verification is the chain
+    rule, decision for decision."""
+    from oracle import accept_tree_sequential
+    rng = np.random.default_rng(9)
+    V, k = 16, 4
+    for _ in range(200):
+        p_rows = np.stack([_dist(V, rng) for _ in range(k + 1)])
+        q_rows = np.stack([_dist(V, rng) for _ in range(k)])
+        toks = [int(rng.integers(V)) for _ in range(k)]
+        us = list(rng.random(k + 1))
+        a = accept_chain(p_rows, q_rows, toks, us)
+        b = accept_tree_sequential(p_rows, {j: q_rows[j] for j in range(k)}, toks, us, [-1, 0, 1, 2, 3])
+        assert (a["accepted_len"], a["next_token"]) == (b["accepted_len"], b["next_token"])
+
+
+def test_sequential_siblings_by_hand():
+    """p = (.5, .3, .2), q = (.2, .5, .3), both children draft token 1.  Child
+    1: u = .7, .7 * .5 = .35 >= .3, rejected; p' = norm(max(0, p - q)) =
+    (1, 0, 0).  Child 2: p'(1) = 0, rejected; p'' = norm(max(0, p' - q)) =
+    (1, 0, 0).  The final token is 0, at the root."""
+    from oracle import accept_tree_sequential
+    p0, q0 = np.array([0.5, 0.3, 0.2]), np.array([0.2, 0.5, 0.3])
+    rows = np.stack([p0, p0, p0])
+    r = accept_tree_sequential(rows, {0: q0}, [1, 1], [0.7, 0.1, 0.5], [-1, 0, 0])
+    assert (r["accepted_len"], r["accepted_node"], r["next_token"]) == (0, 0, 0)
+    # u = .5 accepts child 1 (.25 < .3): the bonus comes from row 1
+    rows2 = np.stack([p0, np.array([0.0, 0.0, 1.0]), p0])
+    r = accept_tree_sequential(rows2, {0: q0}, [1, 1], [0.5, 0.1, 0.5], [-1, 0, 0])
+    assert (r["accepted_len"], r["accepted_node"], r["next_token"]) == (1, 1, 2)
