@@ -65,7 +65,7 @@ extern "C" {
 #define SPEC_API
 #endif
 
-#define SPEC_ABI_VERSION 3
+#define SPEC_ABI_VERSION 4
 #define SPEC_MAX_DRAFT 16        /* chain drafts per request */
 #define SPEC_MAX_TREE_NODES 32   /* token-tree nodes per request, root included */
 
@@ -76,6 +76,11 @@ typedef enum spec_status {
   SPEC_ERR_WORKSPACE = 3,     /* workspace or staging too small or misaligned */
   SPEC_ERR_HIP = 4            /* a HIP runtime call failed (launch, copy) */
 } spec_status_t;
+
+typedef enum spec_tree_rule {
+  SPEC_TREE_INDEPENDENT = 0,
+  SPEC_TREE_SEQUENTIAL = 1
+} spec_tree_rule_t;
 
 typedef enum spec_dtype {
   SPEC_F32 = 0,
@@ -182,10 +187,23 @@ typedef struct spec_attn_args {
  *   next_token    [B] out: the token sampled after the accepted prefix.
  *   accepted_node [B] out (may be NULL): the deepest accepted node (chain:
  *                 equals accepted_len).
- * Tree reading: node n is accepted iff its parent is and its own test
- * passes against the parent's target and draft rows; the deepest accepted
- * node wins, the smallest BFS index on ties; the final token is drawn from
- * that node's target row if it is a leaf, else from the residual.
+ * Tree rules (tree_rule; ignored for chains):
+ *   SPEC_TREE_INDEPENDENT (0): node n is accepted iff its parent is and its
+ *     own test passes against the parent's target and draft rows; the
+ *     deepest accepted node wins, the smallest BFS index on ties; the final
+ *     token is drawn from that node's target row if it is a leaf, else from
+ *     the residual.
+ *   SPEC_TREE_SEQUENTIAL (1): SpecInfer's sequential sibling verification
+ *     (multi-step speculative sampling; the token-tree system the paper's
+ *     evaluation follows, Sec. 5.1), which emits tokens distributed exactly
+ *     as the target when each node's children are drafted i.i.d. from its
+ *     draft row.  From the root, the current node's children are tested in
+ *     BFS order against a running distribution p' (first the node's target
+ *     row): child c is accepted iff u_c * q(x_c) < p'(x_c); a rejection
+ *     replaces p' by max(0, p' - q) normalised (unchanged if that has zero
+ *     mass).  The first accepted child becomes the current node; when none
+ *     is, or the node is a leaf, the final token is drawn from p'.
+ *     accepted_node is the last current node, accepted_len its depth.
  * Inverse-CDF convention: token ids ascending, the smallest id whose
  * cumulative weight exceeds u * (total weight); zero weights never chosen.
  */
@@ -208,6 +226,8 @@ typedef struct spec_accept_args {
   void* event_begin;
   void* event_end;
   void* event_mid;
+  int32_t tree_rule;   /* SPEC_TREE_INDEPENDENT (0) or SPEC_TREE_SEQUENTIAL (1) */
+  int32_t pad0;
 } spec_accept_args_t;
 
 /* Workspace sizes for a call with these arguments (either args pointer may

@@ -65,7 +65,7 @@ class DeviceBatch:
         a.split_kv = split_kv
         return a
 
-    def accept_args(self, with_node: bool = True) -> B.SpecAcceptArgs:
+    def accept_args(self, with_node: bool = True, tree_rule: int = 0) -> B.SpecAcceptArgs:
         p = self.pool
         a = B.SpecAcceptArgs()
         a.vocab = p.vocab
@@ -77,6 +77,7 @@ class DeviceBatch:
         a.uniforms = _ptr(self.uniforms)
         a.accepted_len, a.next_token = _ptr(self.accepted_len), _ptr(self.next_token)
         a.accepted_node = _ptr(self.accepted_node) if with_node else None
+        a.tree_rule = tree_rule
         return a
 
 

@@ -14,6 +14,7 @@ LIB_PATH = os.path.join(_HERE, "libspecverify.so")
 
 SPEC_OK, SPEC_ERR_INVALID_ARG, SPEC_ERR_UNSUPPORTED, SPEC_ERR_WORKSPACE, SPEC_ERR_HIP = range(5)
 SPEC_F32, SPEC_BF16 = 0, 1
+SPEC_TREE_INDEPENDENT, SPEC_TREE_SEQUENTIAL = 0, 1
 SPEC_MAX_DRAFT = 16
 SPEC_MAX_TREE_NODES = 32
 
@@ -73,7 +74,9 @@ class SpecAcceptArgs(C.Structure):
                 ("accepted_node", C.c_void_p),
                 ("event_begin", C.c_void_p),
                 ("event_end", C.c_void_p),
-                ("event_mid", C.c_void_p)]
+                ("event_mid", C.c_void_p),
+                ("tree_rule", C.c_int32),
+                ("pad0", C.c_int32)]
 
 
 class SpecSchedParams(C.Structure):

@@ -366,6 +366,166 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   }
 }
 
+// Sequential sibling verification over a token tree (SpecInfer's multi-step
+// speculative sampling), one work-group per request.  At the current node
+// the children (BFS order) are tested against a running target distribution
+// p', evaluated per token as
+//   p'_0(v) = exp(l(v) - M) / Z,   p'_{j+1}(v) = max(0, p'_j(v) - q(v)) / S_{j+1},
+// where S_{j+1} is the vocabulary sum of max(0, p'_j - q), taken by one
+// coalesced fp64 pass after each rejection (a zero sum, reachable only
+// through rounding, leaves p' as it is).  The first accepted child becomes
+// the current node; when none is, or the node is a leaf, the final token is
+// the smallest id whose cumulative p' exceeds u * (its total), found by a
+// chunked scan in token order (fp64).
+template <typename T>
+__global__ __launch_bounds__(kAccThreads) void acc_tree_seq(AccParams p) {
+  constexpr int G8 = 8;                          // consecutive entries per thread per chunk
+  constexpr int CH = kAccThreads * G8;
+  __shared__ float s_M[kMaxNodes];
+  __shared__ double s_Z[kMaxNodes];
+  __shared__ double s_S[kMaxNodes];
+  __shared__ double redd[4];
+  __shared__ double s_chunk[kAccMaxChunks * kAccChunk / (kAccThreads * 8)];
+  __shared__ double s_tsum[kAccThreads];
+  __shared__ double s_run, s_target;
+  __shared__ int s_pos[4];
+  __shared__ int s_pick;
+  const int i = blockIdx.x;
+  const int tid = threadIdx.x, wv = tid >> 6, ln = tid & 63;
+  const ReqInfo rq = p.reqs[i];
+  const int N = rq.nq;
+  const T* L = static_cast<const T*>(p.logits);
+  const T* Q = static_cast<const T*>(p.probs);
+
+  // (M, Z) of every row of the request, as in the decision kernel
+  for (int r = wv; r < N; r += kAccThreads / 64) {
+    const ChunkStat* st = p.rowstats + (int64_t)(rq.q0 + r) * p.nch;
+    float m = -INFINITY;
+    for (int k = ln; k < p.nch; k += 64) m = fmaxf(m, st[k].m);
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    double z = 0.0;
+    for (int k = ln; k < p.nch; k += 64) z += st[k].s * exp((double)st[k].m - (double)m);
+    for (int o = 32; o >= 1; o >>= 1) z += __shfl_xor(z, o);
+    if (ln == 0) {
+      s_M[r] = m;
+      s_Z[r] = z;
+    }
+  }
+  __syncthreads();
+
+  int node = 0, k = 0;                         // current node, rejections at it (uniform)
+  const T* Lr = L;
+  const T* Qr = Q;
+  bool has_q = false;
+  float M = 0.f;
+  double invZ = 1.0;
+  // running distribution at token v from its logit l and draft probability q
+  auto prun = [&](float l, float q) -> double {
+    double x = (double)expf(l - M) * invZ;
+    for (int j = 0; j < k; ++j) x = fmax(0.0, x - (double)q) / s_S[j];
+    return x;
+  };
+  for (;;) {
+    M = s_M[node];
+    invZ = 1.0 / s_Z[node];
+    Lr = L + (int64_t)(rq.q0 + node) * p.l_st;
+    const int qr = node_qrank(p, node, N);
+    has_q = qr >= 0;
+    Qr = Q + (int64_t)(rq.d0 + (has_q ? qr : 0)) * p.p_st;
+    k = 0;
+    int next = -1;
+    for (int c = node + 1; c < N && next < 0; ++c) {
+      if (node_parent(p, c) != node) continue;
+      // every thread reads the same token, logit, probability and uniform
+      const int x = min(max(p.tokens[rq.q0 - i + c - 1], 0), p.V - 1);
+      const double px = prun(ld(Lr, x), ld(Qr, x));
+      const float qx = ld(Qr, x);
+      if ((double)p.uniforms[rq.q0 + c - 1] * (double)qx < px) {
+        next = c;
+        break;
+      }
+      // rejected: the normaliser of max(0, p' - q)
+      double part = 0.0;
+      for (int b = tid * G8; b < p.V; b += CH)
+        for (int e = 0; e < G8 && b + e < p.V; ++e) {
+          const float q = ld(Qr, b + e);
+          part += fmax(0.0, prun(ld(Lr, b + e), q) - (double)q);
+        }
+      const double S = block_sum(part, redd);
+      if (S > 0.0) {
+        if (tid == 0) s_S[k] = S;
+        __syncthreads();
+        ++k;
+      }
+    }
+    if (next < 0) break;
+    node = next;
+  }
+
+  // The final token from p' at `node`.  Chunk totals (block sums) and the
+  // last id with positive weight first; then one thread walks the chunk
+  // totals, the chosen chunk's per-thread sums and that thread's entries in
+  // token order, so every boundary comes from one sequence of fp64 sums.
+  auto w_at = [&](int v) -> double { return prun(ld(Lr, v), has_q ? ld(Qr, v) : 0.f); };
+  const int nchunk = (p.V + CH - 1) / CH;
+  int last = -1;
+  for (int ch = 0; ch < nchunk; ++ch) {
+    const int b = ch * CH + tid * G8;
+    double part = 0.0;
+    for (int e = 0; e < G8 && b + e < p.V; ++e) {
+      const double w = w_at(b + e);
+      part += w;
+      if (w > 0.0) last = b + e;
+    }
+    const double tot = block_sum(part, redd);
+    if (tid == 0) s_chunk[ch] = tot;
+  }
+  for (int o = 32; o >= 1; o >>= 1) last = max(last, __shfl_xor(last, o));
+  if (ln == 0) s_pos[wv] = last;
+  __syncthreads();
+  if (tid == 0) {
+    double total = 0.0;
+    for (int ch = 0; ch < nchunk; ++ch) total += s_chunk[ch];
+    const double target = (double)p.uniforms[rq.q0 + N - 1] * total;
+    double run = 0.0;
+    int pick = -1;
+    for (int ch = 0; ch < nchunk && pick < 0; ++ch) {
+      if (run + s_chunk[ch] > target) pick = ch;
+      else run += s_chunk[ch];
+    }
+    s_pick = pick;
+    s_run = run;
+    s_target = target;
+  }
+  __syncthreads();
+  int v = -1;
+  if (s_pick >= 0) {
+    const int b = s_pick * CH + tid * G8;
+    double part = 0.0;
+    for (int e = 0; e < G8 && b + e < p.V; ++e) part += w_at(b + e);
+    s_tsum[tid] = part;
+    __syncthreads();
+    if (tid == 0) {
+      const double target = s_target;
+      double c = s_run;
+      int t = 0;
+      while (t < kAccThreads - 1 && !(c + s_tsum[t] > target)) c += s_tsum[t++];
+      const int bt = s_pick * CH + t * G8;
+      for (int e = 0; e < G8 && bt + e < p.V && v < 0; ++e) {
+        c += w_at(bt + e);
+        if (c > target) v = bt + e;
+      }
+    }
+  }
+  if (tid == 0) {
+    // a target at or past the total (rounding): the last id with positive weight
+    if (v < 0) v = max(max(s_pos[0], s_pos[1]), max(s_pos[2], s_pos[3]));
+    p.acc_len[i] = node_depth(p, node);
+    p.next_tok[i] = v;
+    if (p.acc_node) p.acc_node[i] = node;
+  }
+}
+
 // One work-group: every request's draft tokens, their draft probabilities
 // and the uniforms, against the caller's contract (debug builds of a call).
 template <typename T>
@@ -409,6 +569,11 @@ hipError_t launch_rowstats(const AccParams& p, hipStream_t s) {
 
 hipError_t launch_decide(const AccParams& p, hipStream_t s) {
   dim3 block(kAccThreads);
+  if (p.tree == 2) {                       // sequential sibling verification
+    if (p.bf16) acc_tree_seq<uint16_t><<<dim3(p.B), block, 0, s>>>(p);
+    else acc_tree_seq<float><<<dim3(p.B), block, 0, s>>>(p);
+    return hipGetLastError();
+  }
   if (p.bf16) acc_decide_select<uint16_t><<<dim3(p.B * p.nch), block, 0, s>>>(p);
   else acc_decide_select<float><<<dim3(p.B * p.nch), block, 0, s>>>(p);
   return hipGetLastError();

@@ -110,6 +110,7 @@ spec_status_t check_accept(const spec_accept_args_t* a, int64_t Nq, int B) {
     return SPEC_ERR_INVALID_ARG;
   if (a->draft_probs && (a->probs_stride < a->vocab || a->probs_stride % vec || !aligned16(a->draft_probs)))
     return SPEC_ERR_INVALID_ARG;
+  if (a->tree_rule != SPEC_TREE_INDEPENDENT && a->tree_rule != SPEC_TREE_SEQUENTIAL) return SPEC_ERR_INVALID_ARG;
   return SPEC_OK;
 }
 
@@ -508,7 +509,7 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     c.nch = P.nch;
     c.B = P.B;
     c.Nq = (int32_t)P.Nq;
-    c.tree = P.tree ? 1 : 0;
+    c.tree = P.tree ? (acc->tree_rule == SPEC_TREE_SEQUENTIAL ? 2 : 1) : 0;   // 2: sequential siblings
     c.bf16 = acc->dtype == SPEC_BF16;
   }
 

@@ -154,6 +154,8 @@ def test_attention_checks(lib, kw, expect):
     (dict(dtype=B.SPEC_BF16, logits_stride=1008, probs_stride=1008), B.SPEC_OK),
     (dict(target_logits=FAKE + 4), B.SPEC_ERR_INVALID_ARG),
     (dict(dtype=3), B.SPEC_ERR_INVALID_ARG),
+    (dict(tree_rule=2), B.SPEC_ERR_INVALID_ARG),
+    (dict(tree_rule=B.SPEC_TREE_SEQUENTIAL), B.SPEC_OK),
 ])
 def test_accept_checks(lib, kw, expect):
     assert _ws(_req(), None, _acc(**kw))[0] == expect
