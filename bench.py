@@ -248,6 +248,7 @@ def main():
     import numpy as np
     import torch
 
+    from paper_2505_17074_amd import binding as B
     from paper_2505_17074_amd import workload as W
     from paper_2505_17074_amd.batch import DeviceBatch, Verifier
 
@@ -360,6 +361,18 @@ def main():
         ver.run("accept", stream)
     torch.cuda.synchronize()
     t_acc_warm_us = float(np.mean([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)]) * 1e3)
+    # token trees: the acceptance alone (cold) under sequential sibling verification
+    t_acc_seq_us = None
+    if pool.tree_parent is not None:
+        ver.acc.tree_rule = B.SPEC_TREE_SEQUENTIAL
+        for k in range(K):
+            flush()
+            ver.acc.event_begin, ver.acc.event_end = ev[k][2].cuda_event, ev[k][3].cuda_event
+            ver.run("accept", stream)
+        torch.cuda.synchronize()
+        ver.acc.tree_rule = B.SPEC_TREE_INDEPENDENT
+        ver.acc.event_begin = ver.acc.event_end = None
+        t_acc_seq_us = float(np.mean([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)]) * 1e3)
     # the row-statistics kernel alone (cold), in a loop of its own (an event
     # between the two acceptance kernels would lengthen the total above)
     for k in range(K):
@@ -419,6 +432,7 @@ def main():
         "cold": {"steps": KF, "step_us_median": float(np.median(cold)), "step_us_p10": pct(cold, 10),
                  "step_us_p90": pct(cold, 90), "verified_tokens_per_s": work["Nq"] / (float(np.median(cold)) * 1e-6)},
         "accept": {"kernels_us": t_acc_us, "kernels_us_warm": t_acc_warm_us,
+                   "kernels_us_sequential_tree": t_acc_seq_us,
                    "algorithmic_bytes_upper": work["accept_bytes"],
                    "achieved_GBs": work["accept_bytes"] / (t_acc_us * 1e-6) / 1e9,
                    "frac": work["accept_bytes"] / (t_acc_us * 1e-6) / 1e9 / HBM_PEAK_GBS,

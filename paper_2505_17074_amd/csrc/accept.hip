@@ -367,28 +367,47 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
 }
 
 // Sequential sibling verification over a token tree (SpecInfer's multi-step
-// speculative sampling), one work-group per request.  At the current node
-// the children (BFS order) are tested against a running target distribution
-// p', evaluated per token as
+// speculative sampling), one 1024-thread work-group per request.  At the
+// current node the children (BFS order) are tested against a running target
+// distribution p', evaluated per token as
 //   p'_0(v) = exp(l(v) - M) / Z,   p'_{j+1}(v) = max(0, p'_j(v) - q(v)) / S_{j+1},
 // where S_{j+1} is the vocabulary sum of max(0, p'_j - q), taken by one
-// coalesced fp64 pass after each rejection (a zero sum, reachable only
-// through rounding, leaves p' as it is).  The first accepted child becomes
-// the current node; when none is, or the node is a leaf, the final token is
-// the smallest id whose cumulative p' exceeds u * (its total), found by a
-// chunked scan in token order (fp64).
+// coalesced fp64 pass (16-byte loads, several chunks in flight) after each
+// rejection and applied as its reciprocal (within an ulp of the division);
+// a zero sum, reachable only through rounding, leaves p' as it is.  Each
+// child's test inputs (token, the parent row's logit and draft probability
+// there, uniform) do not depend on the walk and are loaded up front.  The first accepted
+// child becomes the current node; when none is, or the node is a leaf, the
+// final token is the smallest id whose cumulative p' exceeds u * (its total).
+constexpr int kSeqThreads = 1024;
+
+template <int NW>
+__device__ __forceinline__ double block_sum_n(double x, double* red) {
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  double s = 0.0;
+  for (int w = 0; w < NW; ++w) s += red[w];
+  return s;
+}
+
 template <typename T>
-__global__ __launch_bounds__(kAccThreads) void acc_tree_seq(AccParams p) {
-  constexpr int G8 = 8;                          // consecutive entries per thread per chunk
-  constexpr int CH = kAccThreads * G8;
+__global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
+  constexpr int NW = kSeqThreads / 64;
+  constexpr int VW = 16 / sizeof(T);            // entries per 16-byte load
+  constexpr int CH = kSeqThreads * VW;          // entries per chunk
+  constexpr int UNR = 16 / VW;                  // chunks whose loads are in flight together (16 entries)
   __shared__ float s_M[kMaxNodes];
   __shared__ double s_Z[kMaxNodes];
-  __shared__ double s_S[kMaxNodes];
-  __shared__ double redd[4];
-  __shared__ double s_chunk[kAccMaxChunks * kAccChunk / (kAccThreads * 8)];
-  __shared__ double s_tsum[kAccThreads];
+  __shared__ double s_iS[kMaxNodes];           // 1 / S_j at the current node
+  __shared__ float s_lx[kMaxNodes], s_qx[kMaxNodes], s_u[kMaxNodes];
+  __shared__ double redd[NW];
+  __shared__ double s_chunk[kAccMaxChunks * kAccChunk / (kSeqThreads * 4)];
+  __shared__ double s_tsum[kSeqThreads];
+  __shared__ double s_wtot[NW];
   __shared__ double s_run, s_target;
-  __shared__ int s_pos[4];
+  __shared__ int s_pos[NW];
   __shared__ int s_pick;
   const int i = blockIdx.x;
   const int tid = threadIdx.x, wv = tid >> 6, ln = tid & 63;
@@ -397,8 +416,18 @@ __global__ __launch_bounds__(kAccThreads) void acc_tree_seq(AccParams p) {
   const T* L = static_cast<const T*>(p.logits);
   const T* Q = static_cast<const T*>(p.probs);
 
+  // every child's test inputs, which do not depend on the walk: its token,
+  // its parent's logit and draft probability there, and its uniform
+  if (tid >= 1 && tid < N) {
+    const int par = node_parent(p, tid);
+    const int x = min(max(p.tokens[rq.q0 - i + tid - 1], 0), p.V - 1);
+    const int qr = node_qrank(p, par, N);
+    s_lx[tid] = ld(L + (int64_t)(rq.q0 + par) * p.l_st, x);
+    s_qx[tid] = qr >= 0 ? ld(Q + (int64_t)(rq.d0 + qr) * p.p_st, x) : 0.f;
+    s_u[tid] = p.uniforms[rq.q0 + tid - 1];
+  }
   // (M, Z) of every row of the request, as in the decision kernel
-  for (int r = wv; r < N; r += kAccThreads / 64) {
+  for (int r = wv; r < N; r += NW) {
     const ChunkStat* st = p.rowstats + (int64_t)(rq.q0 + r) * p.nch;
     float m = -INFINITY;
     for (int k = ln; k < p.nch; k += 64) m = fmaxf(m, st[k].m);
@@ -419,11 +448,19 @@ __global__ __launch_bounds__(kAccThreads) void acc_tree_seq(AccParams p) {
   bool has_q = false;
   float M = 0.f;
   double invZ = 1.0;
-  // running distribution at token v from its logit l and draft probability q
+  // running distribution at a token from its logit l and draft probability q
   auto prun = [&](float l, float q) -> double {
     double x = (double)expf(l - M) * invZ;
-    for (int j = 0; j < k; ++j) x = fmax(0.0, x - (double)q) / s_S[j];
+    for (int j = 0; j < k; ++j) x = fmax(0.0, x - (double)q) * s_iS[j];
     return x;
+  };
+  // this thread's VW entries starting at v: logits (-inf past V) and draft
+  // probabilities (0 past V, or everywhere for a node without a draft row)
+  auto load = [&](int v, float* l, float* q) {
+    load_vec(Lr, v, p.V, -INFINITY, l);
+    if (has_q) load_vec(Qr, v, p.V, 0.f, q);
+    else
+      for (int e = 0; e < VW; ++e) q[e] = 0.f;
   };
   for (;;) {
     M = s_M[node];
@@ -436,24 +473,26 @@ __global__ __launch_bounds__(kAccThreads) void acc_tree_seq(AccParams p) {
     int next = -1;
     for (int c = node + 1; c < N && next < 0; ++c) {
       if (node_parent(p, c) != node) continue;
-      // every thread reads the same token, logit, probability and uniform
-      const int x = min(max(p.tokens[rq.q0 - i + c - 1], 0), p.V - 1);
-      const double px = prun(ld(Lr, x), ld(Qr, x));
-      const float qx = ld(Qr, x);
-      if ((double)p.uniforms[rq.q0 + c - 1] * (double)qx < px) {
+      const float qx = s_qx[c];
+      const double px = prun(s_lx[c], qx);
+      if ((double)s_u[c] * (double)qx < px) {
         next = c;
         break;
       }
-      // rejected: the normaliser of max(0, p' - q)
+      // rejected: the normaliser of max(0, p' - q), UNR chunks' loads in flight
       double part = 0.0;
-      for (int b = tid * G8; b < p.V; b += CH)
-        for (int e = 0; e < G8 && b + e < p.V; ++e) {
-          const float q = ld(Qr, b + e);
-          part += fmax(0.0, prun(ld(Lr, b + e), q) - (double)q);
-        }
-      const double S = block_sum(part, redd);
+      for (int b = 0; b < p.V; b += CH * UNR) {
+        float l[UNR][VW], q[UNR][VW];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) load(b + u * CH + tid * VW, l[u], q[u]);
+#pragma unroll
+        for (int u = 0; u < UNR; ++u)
+#pragma unroll
+          for (int e = 0; e < VW; ++e) part += fmax(0.0, prun(l[u][e], q[u][e]) - (double)q[u][e]);
+      }
+      const double S = block_sum_n<NW>(part, redd);
       if (S > 0.0) {
-        if (tid == 0) s_S[k] = S;
+        if (tid == 0) s_iS[k] = 1.0 / S;
         __syncthreads();
         ++k;
       }
@@ -466,19 +505,28 @@ __global__ __launch_bounds__(kAccThreads) void acc_tree_seq(AccParams p) {
   // last id with positive weight first; then one thread walks the chunk
   // totals, the chosen chunk's per-thread sums and that thread's entries in
   // token order, so every boundary comes from one sequence of fp64 sums.
-  auto w_at = [&](int v) -> double { return prun(ld(Lr, v), has_q ? ld(Qr, v) : 0.f); };
   const int nchunk = (p.V + CH - 1) / CH;
   int last = -1;
-  for (int ch = 0; ch < nchunk; ++ch) {
-    const int b = ch * CH + tid * G8;
-    double part = 0.0;
-    for (int e = 0; e < G8 && b + e < p.V; ++e) {
-      const double w = w_at(b + e);
-      part += w;
-      if (w > 0.0) last = b + e;
+  for (int c0 = 0; c0 < nchunk; c0 += UNR) {
+    float l[UNR][VW], q[UNR][VW];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) load((c0 + u) * CH + tid * VW, l[u], q[u]);
+    double part[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      part[u] = 0.0;
+#pragma unroll
+      for (int e = 0; e < VW; ++e) {
+        const double w = prun(l[u][e], q[u][e]);
+        part[u] += w;
+        if (w > 0.0) last = (c0 + u) * CH + tid * VW + e;
+      }
     }
-    const double tot = block_sum(part, redd);
-    if (tid == 0) s_chunk[ch] = tot;
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const double tot = block_sum_n<NW>(part[u], redd);
+      if (tid == 0 && c0 + u < nchunk) s_chunk[c0 + u] = tot;
+    }
   }
   for (int o = 32; o >= 1; o >>= 1) last = max(last, __shfl_xor(last, o));
   if (ln == 0) s_pos[wv] = last;
@@ -500,26 +548,42 @@ __global__ __launch_bounds__(kAccThreads) void acc_tree_seq(AccParams p) {
   __syncthreads();
   int v = -1;
   if (s_pick >= 0) {
-    const int b = s_pick * CH + tid * G8;
-    double part = 0.0;
-    for (int e = 0; e < G8 && b + e < p.V; ++e) part += w_at(b + e);
-    s_tsum[tid] = part;
+    {
+      const int vb = s_pick * CH + tid * VW;
+      float l[VW], q[VW];
+      load(vb, l, q);
+      double part = 0.0;
+#pragma unroll
+      for (int e = 0; e < VW; ++e) part += prun(l[e], q[e]);
+      s_tsum[tid] = part;
+    }
+    __syncthreads();
+    if (ln == 0) {                           // each wave's total, in lane order
+      double w = 0.0;
+      for (int t = 0; t < 64; ++t) w += s_tsum[wv * 64 + t];
+      s_wtot[wv] = w;
+    }
     __syncthreads();
     if (tid == 0) {
       const double target = s_target;
       double c = s_run;
-      int t = 0;
-      while (t < kAccThreads - 1 && !(c + s_tsum[t] > target)) c += s_tsum[t++];
-      const int bt = s_pick * CH + t * G8;
-      for (int e = 0; e < G8 && bt + e < p.V && v < 0; ++e) {
-        c += w_at(bt + e);
-        if (c > target) v = bt + e;
+      int w = 0;
+      while (w < NW - 1 && !(c + s_wtot[w] > target)) c += s_wtot[w++];
+      int t = w * 64;
+      while (t < w * 64 + 63 && !(c + s_tsum[t] > target)) c += s_tsum[t++];
+      const int vb = s_pick * CH + t * VW;
+      float l[VW], q[VW];
+      load(vb, l, q);
+      for (int e = 0; e < VW && v < 0; ++e) {
+        c += prun(l[e], q[e]);
+        if (c > target) v = vb + e;
       }
     }
   }
   if (tid == 0) {
     // a target at or past the total (rounding): the last id with positive weight
-    if (v < 0) v = max(max(s_pos[0], s_pos[1]), max(s_pos[2], s_pos[3]));
+    if (v < 0)
+      for (int w = 0; w < NW; ++w) v = max(v, s_pos[w]);
     p.acc_len[i] = node_depth(p, node);
     p.next_tok[i] = v;
     if (p.acc_node) p.acc_node[i] = node;
@@ -570,8 +634,8 @@ hipError_t launch_rowstats(const AccParams& p, hipStream_t s) {
 hipError_t launch_decide(const AccParams& p, hipStream_t s) {
   dim3 block(kAccThreads);
   if (p.tree == 2) {                       // sequential sibling verification
-    if (p.bf16) acc_tree_seq<uint16_t><<<dim3(p.B), block, 0, s>>>(p);
-    else acc_tree_seq<float><<<dim3(p.B), block, 0, s>>>(p);
+    if (p.bf16) acc_tree_seq<uint16_t><<<dim3(p.B), dim3(kSeqThreads), 0, s>>>(p);
+    else acc_tree_seq<float><<<dim3(p.B), dim3(kSeqThreads), 0, s>>>(p);
     return hipGetLastError();
   }
   if (p.bf16) acc_decide_select<uint16_t><<<dim3(p.B * p.nch), block, 0, s>>>(p);
