@@ -21,6 +21,11 @@
  *   3. outputs: each request's accepted count a_i -- what the scheduler's
  *      acceptance-rate estimate consumes (Sec. 4.3) -- and its next token.
  *
+ * The KV cache is either packed per request or paged through block tables
+ * (spec_attn_args_t); token trees are verified by independent per-node
+ * tests or by sequential sibling verification (spec_accept_args_t).  The
+ * scheduler that consumes a_i has its own ABI in specsched.h.
+ *
  * Conventions for every entry point
  *   - Device pointers point to memory on the current HIP device; host
  *     pointers are read during the call only.  The library keeps no pointer
