@@ -1,6 +1,6 @@
 """Benchmark of the batched speculative-decoding verify step on one MI355X.
 
-A step is one spec_verify call over one batch: host plan + upload, split-KV
+A step is one spec_verify call over one batch: host plan (staged), split-KV
 verify attention (+ combine), acceptance and the final sample -- every row of
 the hot path -- over inputs already resident in HBM.  Prints ONE JSON line.
 
@@ -294,7 +294,7 @@ def main():
     # the attention kernel alone (spec_verify_attn, nothing beside it on the
     # GPU), for its own roofline next to the in-step figure above, where it
     # shares HBM with the acceptance kernels on the side stream; events on the
-    # caller's stream around each call give the whole call (plan upload, split
+    # caller's stream around each call give the whole call (split
     # kernel, split combine)
     for k in range(K):
         ver.attn.event_begin, ver.attn.event_end = ev[k][0].cuda_event, ev[k][1].cuda_event
@@ -416,7 +416,7 @@ def main():
                      "kernel_us_p10": pct(attn_samples, 10), "kernel_us_p90": pct(attn_samples, 90),
                      "kernel_us_alone": t_alone_us,
                      "frac_alone": work["attn_bytes"] / (t_alone_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
-                     # the whole spec_verify_attn call alone: plan upload + split + combine
+                     # the whole spec_verify_attn call alone: split + combine, with their launch gaps
                      "call_us_alone": t_call_us,
                      # the same kernel over a paged KV cache (64-token pages, random order)
                      "paged": {"page_tokens": 64, "kernel_us_alone": t_paged_us,

@@ -35,10 +35,12 @@
  *   - `stream` is a hipStream_t (NULL = the null stream).  All device work
  *     is enqueued on it in order; nothing synchronises the device.  Outputs
  *     are valid once the stream has passed the call.
- *   - The host staging buffer is written by the call and read by an
- *     asynchronous copy on `stream`: it must stay untouched until the stream
- *     has passed the call.  Calls in flight at the same time need separate
- *     workspaces and staging buffers.
+ *   - The host staging buffer is written by the call and read on `stream`:
+ *     when it is pinned (hipHostMalloc), the call's kernels read the plan
+ *     through its device mapping, with no copy ahead of them; otherwise an
+ *     asynchronous copy brings it into the workspace.  Either way it must
+ *     stay untouched until the stream has passed the call.  Calls in flight
+ *     at the same time need separate workspaces and staging buffers.
  *   - All argument checks run on the host before any HIP call; on an error
  *     nothing is enqueued and no output is touched.  Device-resident values
  *     (draft token ids in [0, V), uniforms in [0, 1), a positive draft
@@ -47,8 +49,7 @@
  *     SPEC_DEBUG_VALIDATE is set to a non-empty value other than "0": then
  *     spec_accept and spec_verify first check the first three on the device,
  *     wait for `stream`, and return SPEC_ERR_INVALID_ARG if any fails (the
- *     plan upload and the check are then the only work enqueued, and no
- *     output is touched).  Without the check an out-of-range token id is
+ *     check is then the only work enqueued, and no output is touched).  Without the check an out-of-range token id is
  *     clamped into [0, V): its results are meaningless, but nothing outside
  *     the arguments is read.
  *   - Results are deterministic: the same inputs give bit-identical outputs
@@ -238,7 +239,7 @@ typedef struct spec_accept_args {
 /* Workspace sizes for a call with these arguments (either args pointer may
  * be NULL when that part is not run).  The device workspace must be
  * 256-byte aligned; the host staging buffer should be pinned
- * (hipHostMalloc) for the copy to be asynchronous. */
+ * (hipHostMalloc), so that the kernels read the plan where it was staged. */
 SPEC_API spec_status_t spec_workspace_bytes(const spec_requests_t* req,
                                    const spec_attn_args_t* attn,
                                    const spec_accept_args_t* acc,
@@ -259,10 +260,10 @@ SPEC_API spec_status_t spec_accept(const spec_requests_t* req,
                           void* host_staging, size_t host_staging_bytes,
                           void* stream);
 
-/* The whole verify step with one plan upload.  The logits are inputs, so the
+/* The whole verify step with one staged plan.  The logits are inputs, so the
  * two parts are independent: the acceptance kernels run on a library-owned
  * side stream (one per device, created on first use at the default priority)
- * that forks from `stream` after the upload and is joined back into `stream`
+ * that forks from `stream` at the start of the call and is joined back into `stream`
  * before the call returns, overlapping the attention kernels.  Completion is
  * still ordered by `stream` alone. */
 SPEC_API spec_status_t spec_verify(const spec_requests_t* req,

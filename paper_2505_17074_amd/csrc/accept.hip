@@ -94,8 +94,18 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
   __shared__ double redd[4];
   const int row = blockIdx.x / p.nch, c = blockIdx.x % p.nch;
   const T* lp = static_cast<const T*>(p.logits) + (int64_t)row * p.l_st;
+  // the first B work-groups (the grid has Nq >= B rows) bring request
+  // blockIdx.x's entry of the staged table into device memory and clear its
+  // ticket, for the decision kernel that follows on the stream
+  uint4 rq_half;
+  const bool copier = blockIdx.x < p.B && threadIdx.x < 2;
+  if (copier) rq_half = reinterpret_cast<const uint4*>(p.reqs_src + blockIdx.x)[threadIdx.x];
   float x[16];
   load16_coalesced(lp, c * kAccChunk, p.V, -INFINITY, x);
+  if (copier) {
+    reinterpret_cast<uint4*>(p.reqs + blockIdx.x)[threadIdx.x] = rq_half;
+    if (threadIdx.x == 0) p.tickets[blockIdx.x] = 0;
+  }
   float m = -INFINITY;
 #pragma unroll
   for (int k = 0; k < 16; ++k) m = fmaxf(m, x[k]);
@@ -108,13 +118,13 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
 }
 
 __device__ __forceinline__ int node_parent(const AccParams& p, int n) {
-  return p.tree ? p.topo->parent[n] : n - 1;
+  return p.tree ? p.topo.parent[n] : n - 1;
 }
 __device__ __forceinline__ int node_depth(const AccParams& p, int n) {
-  return p.tree ? p.topo->depth[n] : n;
+  return p.tree ? p.topo.depth[n] : n;
 }
 __device__ __forceinline__ int node_qrank(const AccParams& p, int n, int N) {
-  return p.tree ? p.topo->qrank[n] : (n < N - 1 ? n : -1);
+  return p.tree ? p.topo.qrank[n] : (n < N - 1 ? n : -1);
 }
 
 // Final-sample weight of one entry: residual max(0, p - q) or p itself.
@@ -599,7 +609,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_validate(AccParams p, uint32_
   uint32_t bad = 0u;
   const T* Q = static_cast<const T*>(p.probs);
   for (int i = threadIdx.x; i < p.B; i += kAccThreads) {
-    const ReqInfo rq = p.reqs[i];
+    const ReqInfo rq = p.reqs_src[i];   // runs before the row statistics make the device copy
     for (int n = 0; n < rq.nq; ++n) {
       const float u = p.uniforms[rq.q0 + n];
       if (!(u >= 0.f && u < 1.f)) bad |= 2u;

@@ -35,6 +35,17 @@ __device__ __forceinline__ bool visible(int t, int ctx, uint32_t anc) {
   return t < ctx || ((anc >> (t - ctx)) & 1u);
 }
 
+// The last p.mirror_wg work-groups of the split kernel copy the staged
+// request table and row map into device memory for the split combine (one
+// 16-byte unit per thread and pass).  Each work-group reads its own item from
+// the staged block directly, so nothing else of the plan is copied.
+__device__ __forceinline__ void mirror_plan(const AttnParams& p) {
+  const int k = (int)blockIdx.x - ((int)gridDim.x - p.mirror_wg);
+  if (k < 0) return;
+  const int step = p.mirror_wg * (int)blockDim.x;
+  for (int x = k * (int)blockDim.x + (int)threadIdx.x; x < p.mirror_n16; x += step) p.mirror_dst[x] = p.mirror_src[x];
+}
+
 // ---------------------------------------------------------------------------
 // bf16 MFMA path.  One work-group of W waves per work item; wave w owns query
 // rows 16w .. 16w+15 of the item (W = row tiles).  The waves share 32-key K
@@ -360,6 +371,7 @@ void attn_split_mfma(AttnParams p) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c16 = lane & 15, grp = lane >> 4;
   const AttnItem it = p.items[blockIdx.x];
+  mirror_plan(p);
   const int n = it.nq;
   const int R = it.nheads * n;
   const int ctx = it.ctx;
@@ -551,12 +563,12 @@ __global__ __launch_bounds__(256) void attn_split_valu(AttnParams p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const AttnItem it = p.items[blockIdx.x];
-  const ReqInfo rq = p.reqs[it.req];
-  const int n = rq.nq;
+  mirror_plan(p);
+  const int n = it.nq;
   const int R = it.nheads * n;
-  const int ctx = rq.ctx;
-  const T* Kb = static_cast<const T*>(p.k) + (int64_t)rq.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh;
-  const T* Vb = static_cast<const T*>(p.v) + (int64_t)rq.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh;
+  const int ctx = it.ctx;
+  const T* Kb = static_cast<const T*>(p.k) + (int64_t)it.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh;
+  const T* Vb = static_cast<const T*>(p.v) + (int64_t)it.kv0 * p.kv_st + (int64_t)it.kvh * p.kv_sh;
 
   for (int x = tid; x < RV * D; x += 256) {
     const int r = x / D, e = x % D;
@@ -564,7 +576,7 @@ __global__ __launch_bounds__(256) void attn_split_valu(AttnParams p) {
     if (r < R) {
       const int hh = r / n, j = r - hh * n;
       val = load_elem<T>(static_cast<const T*>(p.q),
-                         (int64_t)(rq.q0 + j) * p.q_st + (int64_t)(it.head_lo + hh) * p.q_sh + e);
+                         (int64_t)(it.q0 + j) * p.q_st + (int64_t)(it.head_lo + hh) * p.q_sh + e);
     }
     qs[r][e] = val;
   }
@@ -592,7 +604,7 @@ __global__ __launch_bounds__(256) void attn_split_valu(AttnParams p) {
       for (int e = 0; e < D; ++e) s += qs[r][e] * ks[lane][e];
       const int j = r % n;
       s *= p.scale_log2;
-      if (t >= it.ke || !visible(t, ctx, p.topo->anc[j])) s = -INFINITY;
+      if (t >= it.ke || !visible(t, ctx, p.anc[j])) s = -INFINITY;
       const float m_old = ml_s[r][0];
       const float m_new = fmaxf(m_old, wave_max(s));
       const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
@@ -627,9 +639,9 @@ __global__ __launch_bounds__(256) void attn_split_valu(AttnParams p) {
     if (r >= R) continue;
     const int hh = r / n, j = r - hh * n, h = it.head_lo + hh;
     if (it.seg < 0) {
-      p.out[((int64_t)(rq.q0 + j) * p.Hq + h) * D + e] = o[x] / ml_s[r][1];
+      p.out[((int64_t)(it.q0 + j) * p.Hq + h) * D + e] = o[x] / ml_s[r][1];
     } else {
-      const int64_t pr = (int64_t)rq.part0 + ((int64_t)it.seg * n + j) * p.Hq + h;
+      const int64_t pr = (int64_t)it.part0 + ((int64_t)it.seg * n + j) * p.Hq + h;
       p.part_o[pr * D + e] = o[x];
       if (e == 0) p.part_ml[pr] = make_float2(ml_s[r][0], ml_s[r][1]);
     }
@@ -715,21 +727,7 @@ hipError_t launch_mfma(const AttnParams& p, int nr, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Plan upload: the staging buffer is pinned host memory mapped into the
-// device address space, read here over the bus (an enqueued kernel, so the
-// host never waits for earlier work on the stream, unlike a small copy).
-__global__ __launch_bounds__(256) void plan_upload(const uint4* __restrict__ src, uint4* __restrict__ dst, int n16) {
-  for (int i = blockIdx.x * 256 + threadIdx.x; i < n16; i += gridDim.x * 256) dst[i] = src[i];
-}
-
 }  // namespace
-
-hipError_t launch_upload(const void* host_mapped, void* dst, size_t bytes, hipStream_t s) {
-  const int n16 = (int)(bytes / 16);
-  const int grid = std::min(64, std::max(1, (n16 + 255) / 256));
-  plan_upload<<<grid, 256, 0, s>>>(static_cast<const uint4*>(host_mapped), static_cast<uint4*>(dst), n16);
-  return hipGetLastError();
-}
 
 int max_rows_per_item(int dtype_bf16, int D) { return dtype_bf16 ? 80 : 4096 / D; }
 

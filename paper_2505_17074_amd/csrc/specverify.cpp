@@ -41,8 +41,9 @@ struct Plan {
   bool has_acc = false;
   int nch = 0;
   // layout (bytes)
-  size_t off_topo = 0, off_reqs = 0, off_items = 0, off_rowreq = 0, plan_bytes = 0;
-  size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_masses = 0, off_tickets = 0, off_flag = 0;
+  size_t off_reqs = 0, off_rowreq = 0, off_items = 0, plan_bytes = 0;
+  size_t off_acc_reqs = 0, off_tickets = 0;
+  size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_masses = 0, off_flag = 0;
   size_t device_bytes = 0;
 };
 
@@ -358,19 +359,23 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
     P.nr_max = nr;
   }
 
-  // layout: the plan block (uploaded), then device-only scratch
+  // Staged block (the caller's pinned staging buffer; the kernels read it in
+  // place): request table, row -> request map, attention items.  The device
+  // workspace starts with room for the same block -- the split combine's
+  // copies of the table and map, or all of it when the staging buffer is
+  // not device-mapped and is copied -- followed by device-only scratch.
   size_t off = 0;
-  P.off_topo = off;
-  off = align_up(off + sizeof(Topo));
   P.off_reqs = off;
   off = align_up(off + sizeof(ReqInfo) * P.B);
-  P.off_items = off;
-  off = align_up(off + sizeof(AttnItem) * P.items.size());
   P.off_rowreq = off;
   off = align_up(off + sizeof(int32_t) * P.Nq);
-  P.off_tickets = off;                 // acceptance tickets, uploaded as zero
-  off = align_up(off + sizeof(int32_t) * (size_t)(P.has_acc ? P.B : 0));
+  P.off_items = off;
+  off = align_up(off + sizeof(AttnItem) * P.items.size());
   P.plan_bytes = off;
+  P.off_acc_reqs = off;                // the acceptance kernels' copy of the table
+  off = align_up(off + sizeof(ReqInfo) * (size_t)(P.has_acc ? P.B : 0));
+  P.off_tickets = off;                 // acceptance tickets, cleared on the device
+  off = align_up(off + sizeof(int32_t) * (size_t)(P.has_acc ? P.B : 0));
   const int D = attn ? attn->head_dim : 0;
   P.off_part_o = off;
   off = align_up(off + sizeof(float) * (size_t)P.parts * D);
@@ -388,7 +393,7 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
 
 // spec_verify runs the acceptance kernels (which read only logits, draft
 // rows, tokens and uniforms) on a side stream forked from the caller's stream
-// after the plan upload and joined back before returning, so they overlap
+// at the start of the call and joined back before returning, so they overlap
 // the attention kernels.  One side stream and one fork/join event pair per
 // device, created on first use at the default priority and kept for the life
 // of the process; the mutex keeps concurrent callers' fork/join pairs apart.
@@ -422,10 +427,8 @@ SideStream* side_stream() {
 
 void write_staging(const Plan& P, void* host) {
   char* h = static_cast<char*>(host);
-  // every section is written whole; the acceptance tickets must start at
-  // zero (alignment padding between sections is never read)
-  std::memset(h + P.off_tickets, 0, P.plan_bytes - P.off_tickets);
-  std::memcpy(h + P.off_topo, &P.topo, sizeof(Topo));
+  // every section is written whole (alignment padding between sections is
+  // copied along with the table and map but never read)
   std::memcpy(h + P.off_reqs, P.reqs.data(), sizeof(ReqInfo) * P.reqs.size());
   if (!P.items.empty()) std::memcpy(h + P.off_items, P.items.data(), sizeof(AttnItem) * P.items.size());
   std::memcpy(h + P.off_rowreq, P.row_req.data(), sizeof(int32_t) * P.row_req.size());
@@ -442,19 +445,17 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* d = static_cast<char*>(ws);
   write_staging(P, staging);
-  // pinned (device-mapped) staging: a kernel pulls the plan; otherwise a copy
+  // The kernels read the plan where it was staged when the staging buffer is
+  // device-mapped pinned memory (no upload pass ahead of them); otherwise it
+  // is copied into the workspace first.
+  const char* pl = d;
   void* mapped = nullptr;
-  if (hipHostGetDevicePointer(&mapped, staging, 0) == hipSuccess && mapped &&
-      (reinterpret_cast<uintptr_t>(mapped) & 15u) == 0) {
-    if (sv::launch_upload(mapped, d, P.plan_bytes, s) != hipSuccess) return SPEC_ERR_HIP;
+  if (hipHostGetDevicePointer(&mapped, staging, 0) == hipSuccess && mapped && aligned16(mapped)) {
+    pl = static_cast<const char*>(mapped);
   } else {
     (void)hipGetLastError();   // clear the lookup's error state
     if (hipMemcpyAsync(d, staging, P.plan_bytes, hipMemcpyHostToDevice, s) != hipSuccess) return SPEC_ERR_HIP;
   }
-
-  const ReqInfo* reqs = reinterpret_cast<const ReqInfo*>(d + P.off_reqs);
-  const Topo* topo = reinterpret_cast<const Topo*>(d + P.off_topo);
-  const int32_t* row_req = reinterpret_cast<const int32_t*>(d + P.off_rowreq);
 
   sv::AttnParams a{};
   if (attn) {
@@ -468,10 +469,18 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     a.out = attn->out;
     a.part_o = reinterpret_cast<float*>(d + P.off_part_o);
     a.part_ml = reinterpret_cast<float2*>(d + P.off_part_ml);
-    a.items = reinterpret_cast<const AttnItem*>(d + P.off_items);
-    a.reqs = reqs;
-    a.topo = topo;
-    a.row_req = row_req;
+    a.items = reinterpret_cast<const AttnItem*>(pl + P.off_items);
+    a.reqs = reinterpret_cast<const ReqInfo*>(d + P.off_reqs);
+    a.row_req = reinterpret_cast<const int32_t*>(d + P.off_rowreq);
+    if (P.parts > 0 && pl != d) {      // the combine runs: mirror its table and map
+      const bool mfma = attn->dtype == SPEC_BF16;
+      const int64_t threads = mfma ? 64 * (int64_t)P.nr_max : 256;
+      const int64_t n16 = (int64_t)(P.off_items / 16);
+      a.mirror_src = reinterpret_cast<const uint4*>(pl);
+      a.mirror_dst = reinterpret_cast<uint4*>(d);
+      a.mirror_n16 = (int32_t)n16;
+      a.mirror_wg = (int32_t)std::min<int64_t>((int64_t)P.items.size(), (n16 + threads - 1) / threads);
+    }
     a.n_parts = (int32_t)P.parts;
     const float scale = attn->scale > 0.f ? attn->scale : 1.f / std::sqrt((float)attn->head_dim);
     a.scale_log2 = scale * 1.4426950408889634f;
@@ -499,9 +508,9 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     c.acc_len = acc->accepted_len;
     c.next_tok = acc->next_token;
     c.acc_node = acc->accepted_node;
-    c.reqs = reqs;
-    c.topo = topo;
-    c.row_req = row_req;
+    c.reqs_src = reinterpret_cast<const ReqInfo*>(pl + P.off_reqs);
+    c.reqs = reinterpret_cast<ReqInfo*>(d + P.off_acc_reqs);
+    c.topo = P.topo;
     c.rowstats = reinterpret_cast<sv::ChunkStat*>(d + P.off_rowstats);
     c.tickets = reinterpret_cast<int32_t*>(d + P.off_tickets);
     c.masses = reinterpret_cast<double*>(d + P.off_masses);

@@ -40,6 +40,9 @@ struct AttnItem {
   int32_t pad[4];
 };
 
+static_assert(sizeof(ReqInfo) == 32, "ReqInfo is copied as two 16-byte units");
+static_assert(sizeof(AttnItem) == 64, "one 64-byte scalar load per work item");
+
 // Tree / chain topology tables (one per step).
 struct Topo {
   uint32_t anc[kMaxNodes];    // ancestors-or-self bit mask of each node
@@ -58,10 +61,19 @@ struct AttnParams {
   float* out;
   float* part_o;      // [P, d] unnormalised partial outputs
   float2* part_ml;    // [P] (running max in log2 units, running sum)
-  const AttnItem* items;
-  const ReqInfo* reqs;
-  const Topo* topo;
+  const AttnItem* items;    // read where the host staged them (see below)
+  const ReqInfo* reqs;      // device copies read by the split combine
   const int32_t* row_req;   // query row -> request
+  // The plan stays in the caller's pinned staging buffer, mapped into the
+  // device address space: each work-group reads its own item from there, so
+  // no upload pass precedes the kernel.  The combine reads the request table
+  // and the row map many times, so the split kernel's last `mirror_wg`
+  // work-groups copy them (mirror_n16 16-byte units, ahead of the items in
+  // the staged block) into device memory first.  mirror_n16 = 0: no copy.
+  const uint4* mirror_src;
+  uint4* mirror_dst;
+  int32_t mirror_n16;
+  int32_t mirror_wg;
   int32_t n_parts;           // rows of the partial buffers
   float scale_log2;   // scale * log2(e)
   int32_t Hq, Hkv, G, D;
@@ -102,15 +114,15 @@ struct AccParams {
   int32_t* acc_len;
   int32_t* next_tok;
   int32_t* acc_node;
-  const ReqInfo* reqs;
-  const Topo* topo;
-  const int32_t* row_req;
+  const ReqInfo* reqs_src;   // request table where the host staged it (mapped pinned memory)
+  ReqInfo* reqs;             // [B] device copy, written by the row-statistics kernel
   ChunkStat* rowstats;   // [Nq, nch]
   double* masses;        // [B, nch] final-sample weight mass per chunk
-  int32_t* tickets;      // [B] chunk masses published per request (zero at launch: uploaded with the plan)
+  int32_t* tickets;      // [B] chunk masses published per request (zeroed by the row-statistics kernel)
   int32_t V, nch, B, Nq;
   int32_t tree;        // 1 = tree mode
   int32_t bf16;
+  Topo topo;           // kernel arguments: node tables without a memory round trip
 };
 
 constexpr int kAccMaxChunks = 1024;    // vocabularies up to 4M entries
@@ -129,7 +141,6 @@ hipError_t launch_decide(const AccParams& p, hipStream_t s);
 // as the OR of 1 (draft token id outside [0, V)), 2 (uniform outside [0, 1))
 // and 4 (draft probability at a draft token not > 0).
 hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_t s);
-hipError_t launch_upload(const void* host_mapped, void* dst, size_t bytes, hipStream_t s);
 hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* out, int blocks, hipStream_t s);
 
 }  // namespace sv
