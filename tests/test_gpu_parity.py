@@ -76,6 +76,36 @@ def test_full_size_sampled(gpu_lib, idx):
     torch.cuda.empty_cache()
 
 
+ODD_VOCAB = [
+    ("vocab_odd_f32", dict(ctx=[1, 2, 3], k=[3, 0, 5], V=4099)),
+    ("vocab_odd_bf16", dict(ctx=[1, 2, 3], k=[3, 0, 5], V=8199, logit=W.BF16)),
+    ("vocab_3", dict(ctx=[1, 2, 3, 4], k=[1, 2, 3, 16], V=3)),
+    ("plain_decode_only", dict(ctx=[5] * 9, k=[0] * 9, V=1000)),
+]
+
+
+@pytest.mark.parametrize("name,kw", ODD_VOCAB, ids=[e[0] for e in ODD_VOCAB])
+def test_accept_padded_rows(gpu_lib, name, kw):
+    """Vocabularies that are not a multiple of a 16-byte load: the rows are
+    stored with a padded stride (NaN in the padding, which must never be
+    read), so one vector load straddles the vocabulary's end."""
+    _say(f"{name} padded rows")
+    pool = U.custom_pool(**kw, seed=hash(name) % 1000)
+    b = DeviceBatch(pool, "cuda")
+    V = pool.vocab
+    vec = 8 if pool.logit_dtype == W.BF16 else 4
+    Vp = -(-V // vec) * vec
+    for attr in ("logits", "probs"):
+        t = getattr(b, attr)
+        if t.numel():
+            pad = torch.full((t.shape[0], Vp + vec), float("nan"), dtype=t.dtype, device=t.device)
+            pad[:, :V] = t
+            setattr(b, attr, pad[:, :V])
+    v = Verifier(b)
+    v.run("accept")
+    _check(pool, v.results(), attn_reqs=[], tag=name)
+
+
 def test_split_invariance(gpu_lib):
     pool = W.make_pool(W.CONFIGS[1], 3, batch=4)
     outs = {}
