@@ -237,6 +237,53 @@ def test_emitted_token_distribution_exact_on_gpu(gpu_lib):
     np.testing.assert_allclose(dist, p0, rtol=0, atol=1e-6)
 
 
+def test_statistical_acceptance_monte_carlo(gpu_lib):
+    """2^20 independent verify rounds through the GPU kernels at vocabulary 8,
+    k = 4, with target and draft rows that do not depend on the prefix:
+      * the mean accepted length matches sum_{j=1..k} prod_{t<j} alpha_t,
+        alpha_t = sum_x min(p_t(x), q_t(x)) (Sec. 4.3: n*A accepted drafts
+        per round), within 5 standard errors;
+      * the first emitted token (the first draft if accepted, else the final
+        sample) follows p_0: chi-square p-value above 1e-6."""
+    from scipy import stats
+    _say("Monte Carlo acceptance, vocab 8, k 4, 2^20 rounds")
+    V, k, B, rounds = 8, 4, 1 << 16, 16
+    rng = np.random.default_rng(23)
+    logits = np.log(rng.dirichlet(np.ones(V), size=k + 1)).astype(np.float32)
+    Q = rng.dirichlet(np.ones(V), size=k).astype(np.float32)
+    pool = U.custom_pool(ctx=[0] * B, k=[k] * B, Hq=1, Hkv=1, d=64, V=V)
+    pool.target_logits[:] = np.tile(logits, (B, 1))
+    pool.draft_probs[:] = np.tile(Q, (B, 1))
+    b = DeviceBatch(pool, "cuda")
+    v = Verifier(b, ring=2, event_every=1)
+    # the distributions the kernels see: p from the stored logits, q as stored
+    P = np.exp(logits.astype(np.float64))
+    P /= P.sum(1, keepdims=True)
+    Qd = Q.astype(np.float64)
+    alpha = np.minimum(P[:k], Qd).sum(1)
+    expect = sum(np.prod(alpha[:j]) for j in range(1, k + 1))
+    acc, first = [], []
+    for _ in range(rounds):
+        toks = np.stack([rng.choice(V, size=B, p=Qd[t] / Qd[t].sum()) for t in range(k)], 1).astype(np.int32)
+        u = (rng.integers(0, 1 << 24, size=(B, k + 1)) * 2.0 ** -24).astype(np.float32)
+        b.tokens.copy_(torch.from_numpy(toks.ravel()))
+        b.uniforms.copy_(torch.from_numpy(u.ravel()))
+        v.run("accept")
+        res = v.results()
+        a = res["accepted_len"].astype(np.int64)
+        assert ((a >= 0) & (a <= k)).all()
+        acc.append(a)
+        first.append(np.where(a >= 1, toks[:, 0], res["next_token"]))
+    a, y = np.concatenate(acc), np.concatenate(first)
+    se = a.std() / np.sqrt(a.size)
+    print(f"mean accepted {a.mean():.5f} closed form {expect:.5f} (se {se:.5f})", flush=True)
+    assert abs(a.mean() - expect) < 5 * se
+    counts = np.bincount(y, minlength=V)
+    chi2, pval = stats.chisquare(counts, P[0] * y.size)
+    print(f"first token chi2 {chi2:.2f} p-value {pval:.3g}", flush=True)
+    assert pval > 1e-6
+
+
 @pytest.mark.parametrize("idx", [1, 2, 3, 4])
 def test_full_size_every_row_written_once_per_run(gpu_lib, idx):
     """Work distribution at full size: the attention kernels hand items out
