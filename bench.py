@@ -389,6 +389,7 @@ def main():
     # tokens a step emits: the accepted drafts plus the final token, per request
     # (the same inputs every step, so the last step's outputs stand for all)
     emitted = int(batch.accepted_len.to(torch.int64).sum().item()) + pool.batch
+    acc_read = W.accept_bytes_read(pool, batch.accepted_node.cpu().numpy())
     # the device's stream ceilings last: their 20 ms of full-rate reads and
     # copies leave the steps that follow them several percent slower
     read_ceiling, copy_rate = stream_ceilings_gbs(dev)
@@ -436,6 +437,10 @@ def main():
                    "algorithmic_bytes_upper": work["accept_bytes"],
                    "achieved_GBs": work["accept_bytes"] / (t_acc_us * 1e-6) / 1e9,
                    "frac": work["accept_bytes"] / (t_acc_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                   # the rows this step's outcome needs (trees: the rows of nodes with
+                   # children, and a chosen leaf's), priced the same way
+                   "bytes_read": acc_read,
+                   "frac_read": acc_read / (t_acc_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
                    # the streaming kernel alone (every target logit once): begin -> mid event
                    "rowstats_us": t_rows_us, "rowstats_bytes": logit_bytes,
                    "rowstats_frac": logit_bytes / (t_rows_us * 1e-6) / 1e9 / HBM_PEAK_GBS},

@@ -19,6 +19,8 @@
 // is accumulated in fp64, and p = e / Z and the residual are formed in fp64.
 // The sampled token then follows the exact inverse CDF except where u * S
 // lies within ~1e-8 (probability mass) of a cumulative boundary.
+#include <algorithm>
+
 #include "sv_internal.h"
 
 namespace sv {
@@ -92,20 +94,30 @@ template <typename T>
 __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
   __shared__ float redf[4];
   __shared__ double redd[4];
-  const int row = blockIdx.x / p.nch, c = blockIdx.x % p.nch;
-  const T* lp = static_cast<const T*>(p.logits) + (int64_t)row * p.l_st;
-  // the first B work-groups (the grid has Nq >= B rows) bring request
+  const int su = blockIdx.x / p.nch, c = blockIdx.x % p.nch;
+  // Under the independent tree rule only the rows of nodes with children:
+  // their normalisers enter the tests, while a leaf's row is needed only when
+  // that leaf is chosen, and the decision kernel then takes its statistics.
+  // Every request has the tree's `nodes` rows there, so the row is arithmetic.
+  int row = su;
+  if (p.tree == 1) {
+    const int ni = p.topo.n_inner;
+    row = (ni > 0 && su < p.B * ni) ? (su / ni) * p.topo.nodes + p.topo.inner[su % ni] : -1;
+  }
+  const T* lp = static_cast<const T*>(p.logits) + (int64_t)max(row, 0) * p.l_st;
+  // the first B work-groups (the grid has at least B of them) bring request
   // blockIdx.x's entry of the staged table into device memory and clear its
   // ticket, for the decision kernel that follows on the stream
   uint4 rq_half;
   const bool copier = blockIdx.x < p.B && threadIdx.x < 2;
   if (copier) rq_half = reinterpret_cast<const uint4*>(p.reqs_src + blockIdx.x)[threadIdx.x];
   float x[16];
-  load16_coalesced(lp, c * kAccChunk, p.V, -INFINITY, x);
+  if (row >= 0) load16_coalesced(lp, c * kAccChunk, p.V, -INFINITY, x);
   if (copier) {
     reinterpret_cast<uint4*>(p.reqs + blockIdx.x)[threadIdx.x] = rq_half;
     if (threadIdx.x == 0) p.tickets[blockIdx.x] = 0;
   }
+  if (row < 0) return;              // uniform: a work-group kept for the copy only
   float m = -INFINITY;
 #pragma unroll
   for (int k = 0; k < 16; ++k) m = fmaxf(m, x[k]);
@@ -148,23 +160,34 @@ __device__ __forceinline__ double load_dev(const double* p) {
 }
 
 // Per (request i, chunk c):
-//   fold the chunk statistics of the request's rows (one wave per row, fixed
-//   reduction order) into fp64 (M, Z); run the tests of Eq. (1) (one lane per
-//   draft node, against its parent's rows); walk to the deepest accepted node;
-//   the chunk's mass of the final-sample weights.  The last of the request's
-//   work-groups to publish its mass (a device-scope ticket) then samples:
-//   prefix over the chunk masses, the chunk holding u * total, an fp64 scan
-//   inside it, the smallest token id whose cumulative weight exceeds u * total.
+//   fold the chunk statistics of the request's rows that have them (one wave
+//   per row, fixed reduction order) into fp64 (M, Z); run the tests of
+//   Eq. (1) (one lane per draft node, against its parent's rows); walk to the
+//   deepest accepted node.  The final sample then weighs the chosen row by
+//   * the residual max(0, p - q) when the node has children (a draft row):
+//     every work-group publishes its chunk's mass of it;
+//   * p itself at a leaf or when every draft is accepted: chunk c's mass is
+//     s_c * exp(m_c - M) from the row's chunk statistics (max m_c, sum s_c of
+//     exp(l - m_c)).  Under the independent tree rule a leaf's row has none
+//     yet, and each work-group takes its chunk's here with the row-statistics
+//     kernel's arithmetic; otherwise only chunk 0's work-group goes on.
+//   The last of the request's work-groups to check in (a device-scope ticket)
+//   samples: prefix over the chunk masses, the chunk holding u * total, an
+//   fp64 scan inside it (for p, in that chunk's units exp(l - m_c)), the
+//   smallest token id whose cumulative weight exceeds the target.
 template <typename T>
 __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   __shared__ double redd[4];
+  __shared__ float redf[4];
   __shared__ float s_M[kMaxNodes];
   __shared__ double s_Z[kMaxNodes];
   __shared__ Decision s_dec;
   __shared__ int s_last;
   __shared__ double s_mass[kAccMaxChunks];
+  __shared__ float s_mc[kAccMaxChunks];
   __shared__ double s_tsum[kAccThreads];
   __shared__ double s_tot, s_base, s_target;
+  __shared__ float s_mrow, s_mcc;
   __shared__ int s_chunk;
   __shared__ int s_cand[4], s_last_pos[4];
   const int i = blockIdx.x / p.nch, c = blockIdx.x % p.nch;
@@ -190,8 +213,9 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
     un = p.uniforms[rq.q0 + n - 1];
   }
 
-  // (M, Z) of every row of the request
+  // (M, Z) of every row of the request that has chunk statistics
   for (int r = wv; r < N; r += kAccThreads / 64) {
+    if (p.tree == 1 && p.topo.qrank[r] < 0) continue;     // a leaf's row: none yet
     const ChunkStat* st = p.rowstats + (int64_t)(rq.q0 + r) * p.nch;
     float m = -INFINITY;
     for (int k = ln; k < p.nch; k += 64) m = fmaxf(m, st[k].m);
@@ -230,8 +254,8 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
       d.row = rq.q0 + best;
       d.qrow = qrank >= 0 ? rq.d0 + qrank : -1;
       d.len = node_depth(p, best);
-      d.M = s_M[best];
-      d.Z = s_Z[best];
+      d.M = qrank >= 0 ? s_M[best] : 0.f;      // the residual's normaliser (a node with children)
+      d.Z = qrank >= 0 ? s_Z[best] : 1.0;
       d.pad = 0.f;
       s_dec = d;
     }
@@ -240,23 +264,47 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   const Decision d = s_dec;
   const double invZ = 1.0 / d.Z;
   bool residual = d.qrow >= 0;
+  const bool own_stats = !residual && p.tree == 1;   // a leaf's row under the independent tree rule
   const T* Lr = L + (int64_t)d.row * p.l_st;
   const T* Qr = Q + (int64_t)(d.qrow >= 0 ? d.qrow : 0) * p.p_st;
-  {
+  ChunkStat* rst = p.rowstats + (int64_t)d.row * p.nch;
+  if (!residual && !own_stats) {
+    // p with the row's statistics at hand: one work-group samples
+    if (c != 0) return;
+    if (tid == 0) s_last = 1;
+  } else {
     float x[16], q[16];
     load16_coalesced(Lr, c * kAccChunk, p.V, -INFINITY, x);
     if (residual) load16_coalesced(Qr, c * kAccChunk, p.V, 0.f, q);
     double sm = 0.0;
+    float m = 0.f;
+    if (residual) {
 #pragma unroll
-    for (int k = 0; k < 16; ++k) sm += final_weight(x[k], residual ? q[k] : 0.f, d.M, invZ, residual);
-    sm = block_sum(sm, redd);
+      for (int k = 0; k < 16; ++k) sm += final_weight(x[k], q[k], d.M, invZ, true);
+      sm = block_sum(sm, redd);
+    } else {
+      // this chunk's statistics of the leaf's row, as the row-statistics kernel takes them
+      m = -INFINITY;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) m = fmaxf(m, x[k]);
+      m = block_max(m, redf);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) sm += (double)expf(x[k] - m);
+      sm = block_sum(sm, redd);
+    }
     if (tid == 0) {
+      if (residual) {
+        if (p.nch == 1) s_mass[0] = sm;
+        else store_dev(p.masses + (int64_t)i * p.nch + c, sm);
+      } else {
+        store_dev(&rst[c].s, sm);
+        __hip_atomic_store(reinterpret_cast<uint32_t*>(&rst[c].m), __float_as_uint(m), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
       if (p.nch == 1) {
-        s_mass[0] = sm;
         s_last = 1;
       } else {
-        store_dev(p.masses + (int64_t)i * p.nch + c, sm);
-        __builtin_amdgcn_s_waitcnt(0);     // the store has reached the device coherence point
+        __builtin_amdgcn_s_waitcnt(0);     // the stores have reached the device coherence point
         const int t = __hip_atomic_fetch_add(p.tickets + i, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         s_last = (t == p.nch - 1);
       }
@@ -266,33 +314,45 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   if (!s_last) return;              // uniform: another work-group of the request samples
 
   // ---- the request's sampler
-  if (p.nch > 1)
-    for (int k = tid; k < p.nch; k += kAccThreads) s_mass[k] = load_dev(p.masses + (int64_t)i * p.nch + k);
-  __syncthreads();
-  if (tid == 0) {
-    double tot = 0.0;
-    for (int k = 0; k < p.nch; ++k) tot += s_mass[k];
-    s_tot = tot;
+  if (residual) {
+    if (p.nch > 1)
+      for (int k = tid; k < p.nch; k += kAccThreads) s_mass[k] = load_dev(p.masses + (int64_t)i * p.nch + k);
+    __syncthreads();
+    if (tid == 0) {
+      double tot = 0.0;
+      for (int k = 0; k < p.nch; ++k) tot += s_mass[k];
+      s_tot = tot;
+    }
+    __syncthreads();
+    // zero residual mass (reachable only through rounding): sample from p
+    // itself, whose row (a node with children) has its statistics
+    residual = s_tot > 0.0;
   }
-  __syncthreads();
-  // zero residual mass (reachable only through rounding): sample from p itself
-  if (!(s_tot > 0.0)) {
-    residual = false;
-    for (int k = 0; k < p.nch; ++k) {
-      float x[16];
-      load16_coalesced(Lr, k * kAccChunk, p.V, -INFINITY, x);
-      double sm = 0.0;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) sm += final_weight(x[e], 0.f, d.M, invZ, false);
-      sm = block_sum(sm, redd);
-      if (tid == 0) s_mass[k] = sm;
+  if (!residual) {
+    // the chosen row's chunk statistics (device-scope loads: a leaf's were
+    // written by this kernel's work-groups), masses in units of exp(M)
+    for (int k = tid; k < p.nch; k += kAccThreads) {
+      s_mass[k] = load_dev(&rst[k].s);
+      s_mc[k] = __uint_as_float(__hip_atomic_load(reinterpret_cast<const uint32_t*>(&rst[k].m), __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT));
+    }
+    __syncthreads();
+    if (tid == 0) {
+      float mx = -INFINITY;
+      for (int k = 0; k < p.nch; ++k) mx = fmaxf(mx, s_mc[k]);
+      double tot = 0.0;
+      for (int k = 0; k < p.nch; ++k) {
+        s_mass[k] = s_mass[k] * exp((double)s_mc[k] - (double)mx);
+        tot += s_mass[k];
+      }
+      s_tot = tot;
+      s_mrow = mx;                  // the row's max M
     }
     __syncthreads();
   }
   const float u = p.uniforms[rq.q0 + N - 1];
   if (tid == 0) {
-    double tot = 0.0;
-    for (int k = 0; k < p.nch; ++k) tot += s_mass[k];
+    const double tot = s_tot;
     const double target = (double)u * tot;
     double cum = 0.0;
     int chosen = -1, last_pos = 0;
@@ -309,11 +369,21 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
       for (int k = 0; k < chosen; ++k) cum += s_mass[k];
     }
     s_chunk = chosen;
-    s_base = cum;
-    s_target = target;
+    if (residual) {
+      s_mcc = 0.f;
+      s_base = cum;
+      s_target = target;
+    } else {
+      // the scan below runs in the chunk's own units exp(l - m_c)
+      const float mc = s_mc[chosen];
+      s_mcc = mc;
+      s_base = 0.0;
+      s_target = (target - cum) / exp((double)mc - (double)s_mrow);
+    }
   }
   __syncthreads();
   const int cc = s_chunk;
+  const float mcc = s_mcc;
   float x[16], q[16];
   double w[16];
   load16_contiguous(Lr, cc * kAccChunk, p.V, -INFINITY, x);
@@ -321,7 +391,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   double tsum = 0.0;
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
-    w[k] = final_weight(x[k], residual ? q[k] : 0.f, d.M, invZ, residual);
+    w[k] = residual ? final_weight(x[k], q[k], d.M, invZ, true) : (double)expf(x[k] - mcc);
     tsum += w[k];
   }
   // exclusive prefix of the per-thread sums, in thread (= token) order
@@ -636,8 +706,11 @@ hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_
 
 hipError_t launch_rowstats(const AccParams& p, hipStream_t s) {
   dim3 block(kAccThreads);
-  if (p.bf16) acc_rowstats<uint16_t><<<dim3(p.Nq * p.nch), block, 0, s>>>(p);
-  else acc_rowstats<float><<<dim3(p.Nq * p.nch), block, 0, s>>>(p);
+  // independent tree rule: the rows of nodes with children (at least B work-groups)
+  const int64_t rows = p.tree == 1 ? (int64_t)p.B * p.topo.n_inner : (int64_t)p.Nq;
+  const dim3 grid((unsigned)std::max<int64_t>(rows * p.nch, p.B));
+  if (p.bf16) acc_rowstats<uint16_t><<<grid, block, 0, s>>>(p);
+  else acc_rowstats<float><<<grid, block, 0, s>>>(p);
   return hipGetLastError();
 }
 

@@ -237,8 +237,10 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
       P.topo.depth[n] = n == 0 ? 0 : P.topo.depth[r->tree_parent[n]] + 1;
       P.topo.anc[n] = (1u << n) | (n == 0 ? 0u : P.topo.anc[r->tree_parent[n]]);
       P.topo.qrank[n] = has_child[n] ? n_int++ : -1;
+      if (has_child[n]) P.topo.inner[P.topo.qrank[n]] = n;
     }
     P.topo.nodes = tn;
+    P.topo.n_inner = n_int;
   }
 
   // requests

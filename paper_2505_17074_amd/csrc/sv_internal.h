@@ -49,8 +49,10 @@ struct Topo {
   int32_t parent[kMaxNodes];  // -1 for the root
   int32_t qrank[kMaxNodes];   // draft-probability row of a node with children, else -1
   int32_t depth[kMaxNodes];
+  int32_t inner[kMaxNodes];   // the nodes with children, in BFS order (tree mode)
   int32_t nodes;              // tree nodes (tree mode) or 0 (chain)
-  int32_t pad[3];
+  int32_t n_inner;            // nodes with children (tree mode)
+  int32_t pad[2];
 };
 
 struct AttnParams {
@@ -116,7 +118,9 @@ struct AccParams {
   int32_t* acc_node;
   const ReqInfo* reqs_src;   // request table where the host staged it (mapped pinned memory)
   ReqInfo* reqs;             // [B] device copy, written by the row-statistics kernel
-  ChunkStat* rowstats;   // [Nq, nch]
+  ChunkStat* rowstats;   // [Nq, nch]; under the independent tree rule the row-statistics
+                         // kernel fills the rows of nodes with children only, and the
+                         // decision kernel a chosen leaf's row
   double* masses;        // [B, nch] final-sample weight mass per chunk
   int32_t* tickets;      // [B] chunk masses published per request (zeroed by the row-statistics kernel)
   int32_t V, nch, B, Nq;

@@ -360,3 +360,26 @@ def workload_bytes(pool: Pool) -> dict:
     acc_bytes = Nq * V * s_l + B * V * s_l + (Nq - B) * (4 + s_l) + Nq * 4 + 8 * B
     return {"attn_bytes": int(attn_bytes), "attn_flops": int(flops), "accept_bytes": int(acc_bytes),
             "Nq": Nq, "Nkv": Nkv}
+
+
+def accept_bytes_read(pool: Pool, accepted_node: np.ndarray) -> int:
+    """Bytes the acceptance kernels read for this step's outcome (independent
+    rule).  Chains: every target row once.  Trees: the rows of nodes with
+    children once (their normalisers enter the tests), and the chosen node's
+    row where it is a leaf.  Plus the draft row of each chosen node that has
+    children (the residual), the draft ids and their draft probabilities,
+    the uniforms and the outputs."""
+    s_l = 4 if pool.logit_dtype == F32 else 2
+    n_q = pool.n_q
+    Nq, V, B = int(n_q.sum()), pool.vocab, pool.batch
+    node = np.asarray(accepted_node, np.int64)
+    if pool.tree_parent is not None:
+        par = pool.tree_parent
+        inner = np.zeros(len(par), bool)
+        inner[par[1:]] = True
+        rows = B * int(inner.sum()) + int((~inner[node]).sum())
+        qrows = int(inner[node].sum())
+    else:
+        rows = Nq
+        qrows = int((node < pool.draft_len).sum())
+    return int((rows + qrows) * V * s_l + (Nq - B) * (4 + s_l) + Nq * 4 + 8 * B)

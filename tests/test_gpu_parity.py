@@ -193,6 +193,29 @@ def test_p_equals_q_accepts_every_draft(gpu_lib):
     assert np.array_equal(res["accepted_len"], pool.draft_len)
 
 
+@pytest.mark.parametrize("V,logit", [(1000, W.F32), (32000, W.F32), (8200, W.BF16)])
+def test_path_tree_equals_chain(gpu_lib, V, logit):
+    """A tree whose parent array is a path (parent(n) = n - 1) is the chain:
+    bit-identical accepted lengths and next tokens, and the deepest accepted
+    node is the accepted length.  Under the independent tree rule the last
+    node's row is a leaf's, whose chunk statistics the decision kernel takes
+    itself, with the row-statistics kernel's arithmetic."""
+    import copy
+    _say(f"path tree == chain, V={V}")
+    K = 6
+    # target close to the draft (sigma 0.15): about half the requests accept
+    # every draft and sample from the last (leaf) row
+    chain = U.custom_pool(ctx=[3, 40, 7, 90, 1, 0, 12, 33] * 2, k=[K] * 16, V=V, logit=logit, seed=V, sigma=0.15)
+    tree = copy.copy(chain)
+    tree.tree_parent = np.arange(-1, K, dtype=np.int32)
+    a = _run(chain, "accept")
+    b = _run(tree, "accept")
+    assert np.array_equal(a["accepted_len"], b["accepted_len"])
+    assert np.array_equal(a["next_token"], b["next_token"])
+    assert np.array_equal(b["accepted_node"], b["accepted_len"])
+    _check(chain, a, attn_reqs=[], tag="chain")
+
+
 def _cells(breaks):
     b = sorted(set([0.0, 1.0] + [float(x) for x in breaks if 0.0 < x < 1.0]))
     return [((lo + hi) / 2.0, hi - lo) for lo, hi in zip(b[:-1], b[1:])]

@@ -82,3 +82,24 @@ def test_lognormal_context_median():
     small = W.make_pool(cfg, seed=0, batch=8)
     c8, k8, s8 = W.request_lengths(cfg, seed=0, batch=8)
     assert np.array_equal(small.ctx_len, c8) and np.array_equal(small.draft_len, k8)
+
+
+def test_accept_bytes_read_model():
+    """The acceptance read model: chains read every target row and the draft
+    row of each request that rejects; trees read the rows of nodes with
+    children, a chosen leaf's row, and a chosen inner node's draft row."""
+    from paper_2505_17074_amd import workload as W
+    pool = W.make_pool(W.CONFIGS[1], 0, batch=4)
+    V, s = pool.vocab, 4
+    Nq, B = int(pool.n_q.sum()), pool.batch
+    fixed = (Nq - B) * (4 + s) + Nq * 4 + 8 * B
+    k = pool.draft_len.astype(np.int64)
+    assert W.accept_bytes_read(pool, k) == Nq * V * s + fixed                  # every draft accepted
+    assert W.accept_bytes_read(pool, np.zeros(B, np.int64)) == (Nq + B) * V * s + fixed
+    assert W.accept_bytes_read(pool, np.zeros(B, np.int64)) == W.workload_bytes(pool)["accept_bytes"]
+    tree = W.make_pool(W.CONFIGS[4], 0, batch=3)
+    Nq, B, V = int(tree.n_q.sum()), tree.batch, tree.vocab
+    fixed = (Nq - B) * (4 + s) + Nq * 4 + 8 * B
+    # 15-node binary tree: nodes 0..6 have children; a leaf (14), an inner node (2), the root (0)
+    got = W.accept_bytes_read(tree, np.array([14, 2, 0]))
+    assert got == (3 * 7 + 1 + 2) * V * s + fixed
