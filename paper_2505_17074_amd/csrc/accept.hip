@@ -1,19 +1,24 @@
 // Speculative acceptance and final sample for gfx950.
 //
 // Two launches, each streaming what it needs once:
-//   acc_rowstats       every target-logit row in 4096-entry chunks: chunk max
-//                      and chunk sum of exp(l - max)          grid Nq x nch
+//   acc_rowstats       target-logit rows in 4096-entry chunks: chunk max and
+//                      chunk sum of exp(l - max)              grid Nq x nch
+//                      (independent tree rule: only the rows of nodes with
+//                      children, grid B x inner nodes x nch)
 //   acc_decide_select  per (request, chunk): fold the chunk stats of the
 //                      request's rows, run the acceptance tests (one lane per
 //                      draft node), walk to the deepest accepted node, then
-//                      the chunk's mass of the final-sample weights
-//                        w = max(0, p - q)  (residual, node with children)
-//                        w = p              (extra token, leaf / all accepted)
-//                      the request's last work-group to publish its mass then
-//                      takes the prefix over chunk masses, picks the chunk
-//                      holding u * total, scans inside it and emits the
-//                      smallest token id whose cumulative weight exceeds the
-//                      target                                grid B x nch
+//                      the final sample's weights
+//                        w = max(0, p - q)  (residual, node with children):
+//                            each chunk's mass, published
+//                        w = p              (extra token, leaf / all accepted):
+//                            chunk masses from the row's chunk statistics
+//                            (a tree leaf's taken here first)
+//                      the request's last work-group to check in then takes
+//                      the prefix over chunk masses, picks the chunk holding
+//                      u * total, scans inside it and emits the smallest
+//                      token id whose cumulative weight exceeds the target
+//                                                            grid B x nch
 // exp(l - max) is evaluated per entry in fp32 (expf, ~1 ulp), but every sum
 // -- the softmax normaliser Z, chunk masses, prefixes and the in-chunk scan --
 // is accumulated in fp64, and p = e / Z and the residual are formed in fp64.
