@@ -11,6 +11,7 @@ import pytest
 import torch
 
 import parity_util as U
+from paper_2505_17074_amd import binding as B
 from paper_2505_17074_amd import workload as W
 from paper_2505_17074_amd.batch import DeviceBatch, Verifier
 
@@ -117,6 +118,31 @@ def test_split_invariance(gpu_lib):
     base = outs[0]
     for split, res in outs.items():
         np.testing.assert_allclose(res["out"], base["out"], rtol=0, atol=5e-3 * np.abs(base["out"]).max())
+
+
+@pytest.mark.parametrize("cfg_idx,batch", [(2, 24), (4, 6)])
+def test_pageable_staging_matches_pinned(gpu_lib, cfg_idx, batch):
+    """A staging buffer in pageable host memory has no device mapping, so the
+    plan is copied into the workspace before the kernels (instead of being
+    read where it was staged): the outputs must be bit-identical.  The ragged
+    batch splits requests, so the combine's copies are exercised too."""
+    cfg = W.CONFIGS[cfg_idx]
+    _say(f"{cfg.name} b{batch}: pageable staging")
+    pool = W.make_pool(cfg, 2, batch=batch)
+    b = DeviceBatch(pool, "cuda")
+    v = Verifier(b)
+    v.run("verify")
+    ref = v.results()
+    b.out.fill_(float("nan"))
+    b.accepted_len.fill_(-1)
+    b.next_token.fill_(-1)
+    staging = np.zeros(v.staging_bytes + 64, np.uint8)          # pageable
+    h = torch.cuda.current_stream().cuda_stream
+    B.check(B.spec_verify(v.req, v.attn, v.acc, v.ws_ptr, v.ws_bytes, staging.ctypes.data, v.staging_bytes, h),
+            "spec_verify")
+    got = v.results()
+    for key in ref:
+        assert np.array_equal(np.asarray(got[key]).view(np.uint8), np.asarray(ref[key]).view(np.uint8)), key
 
 
 def test_deterministic(gpu_lib):
