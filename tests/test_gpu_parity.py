@@ -145,6 +145,20 @@ def test_pageable_staging_matches_pinned(gpu_lib, cfg_idx, batch):
         assert np.array_equal(np.asarray(got[key]).view(np.uint8), np.asarray(ref[key]).view(np.uint8)), key
 
 
+@pytest.mark.parametrize("batch", [40, 96])
+def test_many_split_requests(gpu_lib, batch):
+    """128-key pieces split nearly every request (40 of 40, 93 of 96): many
+    split requests, each with many pieces, through the split kernel's copies
+    of the plan and the combine."""
+    _say(f"ragged b{batch} split_kv=128")
+    pool = W.make_pool(W.CONFIGS[2], 4, batch=batch)
+    split = int(((pool.ctx_len.astype(np.int64) + pool.n_q) > 128).sum())
+    assert (split <= 64) == (batch == 40), split
+    res = _run(pool, split_kv=128)
+    B = pool.batch
+    _check(pool, res, attn_reqs=sorted({0, 1, B // 2, B - 2, B - 1}), tag=f"b{batch}/split128")
+
+
 def test_deterministic(gpu_lib):
     _say("determinism ragged_gqa b32")
     pool = W.make_pool(W.CONFIGS[2], 5, batch=32)
