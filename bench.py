@@ -4,7 +4,11 @@ A step is one spec_verify call over one batch: host plan (staged), split-KV
 verify attention (+ combine), acceptance and the final sample -- every row of
 the hot path -- over inputs already resident in HBM.  Prints ONE JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu]
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--only] [--no-cpu] [--no-sched]
+
+The headline is the largest single-GPU workload (128 ragged GQA requests);
+the other workloads are measured the same way in the same run and reported
+under "workloads".
 """
 from __future__ import annotations
 
@@ -30,7 +34,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="mha7b_b32")
+    ap.add_argument("--workload", default=HEADLINE,
+                    help="the headline workload (default: the largest that fits one GPU)")
+    ap.add_argument("--only", action="store_true", help="measure the headline workload only (profiler runs)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-sched", action="store_true",
@@ -130,8 +136,6 @@ def scheduler_closed_loop(dev, seed: int) -> dict:
     params = CL.default_params(cfg)
     res = CL.evaluate(reqs, params)
     lat = {pol: r["avg_latency_ms"] for pol, r in res.items()}
-    sweep = {K: simulate(reqs, "laps_sd", CL.default_params(cfg, K=K), log=False)["avg_latency"] / 1000.0
-             for K in (1, 2, 3, 4, 6, 8, 10)}
     reps, t0 = 20, time.perf_counter()
     for _ in range(reps):
         o = simulate(reqs, "laps_sd", params, log=False)
@@ -143,10 +147,8 @@ def scheduler_closed_loop(dev, seed: int) -> dict:
             "rounds_traced": int(traces.shape[1]), "trace_s": t_traces,
             "mean_tokens_per_round": float((traces + 1).mean()),
             "avg_latency_ms": lat,
-            "laps_sd_vs": {pol: lat[pol] / lat["laps_sd"] for pol in ("fcfs", "lp_sjf", "las", "sjf_exact")},
             "switches": {pol: r["switches"] for pol, r in res.items()},
             "laps_sd_perceptible": res["laps_sd"]["perceptible"],
-            "laps_sd_avg_latency_ms_by_K": sweep,
             "native_decision_us": dec_us,
             "kv_swap": {"d2h_GBs": swap["d2h_GBs"], "h2d_GBs": swap["h2d_GBs"],
                         "us_per_token_measured": swap["us_per_token"],
@@ -192,8 +194,9 @@ def kernel_source_digest() -> str:
 
 
 def measured_traffic(workload: str):
-    """HBM bytes per launch of the split-KV kernel from the committed rocprofv3
-    counter summary, if it was taken on the current kernel source."""
+    """HBM bytes per call of the attention kernels (split-KV kernel and split
+    combine) from the committed rocprofv3 counter summary, if it was taken on
+    the current kernel source."""
     path = os.path.join(ROOT, "profiles", f"attn_split_{workload}_traffic.md")
     if not os.path.exists(path):
         return None
@@ -230,38 +233,42 @@ def cpu_baseline(pool, budget_s: float):
         t_used += time.perf_counter() - t0
         done_tokens += n
         m += 1
-    return {"value": done_tokens / t_used, "unit": "verified tokens/s", "cores": int(threads), "cpu_model": cpu_model(),
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):                   # pragma: no cover
+        avail = os.cpu_count() or 1
+    return {"value": done_tokens / t_used, "unit": "verified tokens/s", "cores": int(threads),
+            "cores_available": int(avail), "blas_threads": int(threads), "cpu_model": cpu_model(),
             "kind": "oracle",
             "sample": f"{m} request verifications ({m / pool.batch:.2f} passes over the {pool.batch} requests, "
                       f"{done_tokens} verify tokens), attention + acceptance in fp64 NumPy, {t_used:.1f} s"}
 
 
-def main():
-    args = parse()
-    if args.copy_probe:
-        copy_probe(args.copy_probe)
-        return
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); multi-GPU sharding of the verify step is "
-              "described in the design notes but not built", file=sys.stderr)
-        sys.exit(2)
+HEADLINE = "ragged_gqa_b128"          # the largest workload that fits one GPU
+OTHERS = ("mha7b_b32", "long_gqa_b8", "tree15_b64")
+
+
+def measure_workload(name: str, seed: int, K: int, Wm: int, dev, flush) -> tuple:
+    """Every GPU figure of one workload: warm and cold steps, the attention
+    kernels alone (split + combine, packed and paged), the acceptance
+    kernels alone (cold and warm; the row-statistics kernel alone; the
+    sequential tree rule for trees).  Returns (figures, pool, outputs)."""
     import numpy as np
     import torch
 
     from paper_2505_17074_amd import binding as B
     from paper_2505_17074_amd import workload as W
-    from paper_2505_17074_amd.batch import DeviceBatch, Verifier
+    from paper_2505_17074_amd.batch import DeviceBatch, PagedKV, Verifier
 
-    cfg = W.CONFIG_BY_NAME[args.workload]
-    pool = W.make_pool(cfg, args.seed)
+    cfg = W.CONFIG_BY_NAME[name]
+    print(f"[bench] {name}: drawing the seeded workload", file=sys.stderr, flush=True)
+    pool = W.make_pool(cfg, seed)
     work = W.workload_bytes(pool)
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
     batch = DeviceBatch(pool, dev)
     ver = Verifier(batch)
     stream = torch.cuda.current_stream(dev)
+    print(f"[bench] {name}: timing", file=sys.stderr, flush=True)
 
-    K, Wm = args.steps, args.warmup
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
     for e4 in ev:
         for e in e4:
@@ -273,9 +280,10 @@ def main():
     torch.cuda.synchronize()
 
     # The timed region: K whole steps.  On every EVENT_EVERY-th step the
-    # library records two events immediately around the split-KV attention
-    # kernel on its launch stream (the roofline's kernel time); a marker on
-    # every step would itself cost the step several microseconds.
+    # library records two events on the attention's launch stream, before the
+    # split-KV kernel and after the split combine (the roofline's kernel
+    # time); a marker on every step would itself cost the step several
+    # microseconds.
     sampled = [k for k in range(K) if k % EVENT_EVERY == 0]
     t0 = time.perf_counter()
     for k in range(K):
@@ -291,11 +299,10 @@ def main():
     attn_samples = [ev[k][0].elapsed_time(ev[k][1]) * 1e3 for k in sampled]
     t_attn_us = float(np.mean(attn_samples))
 
-    # the attention kernel alone (spec_verify_attn, nothing beside it on the
-    # GPU), for its own roofline next to the in-step figure above, where it
-    # shares HBM with the acceptance kernels on the side stream; events on the
-    # caller's stream around each call give the whole call (split
-    # kernel, split combine)
+    # the attention kernels alone (spec_verify_attn, nothing beside them on
+    # the GPU), next to the in-step figure above, where they share HBM with
+    # the acceptance kernels on the side stream; events on the caller's
+    # stream around each call give the whole call with its launch gaps
     for k in range(K):
         ver.attn.event_begin, ver.attn.event_end = ev[k][0].cuda_event, ev[k][1].cuda_event
         ev[k][2].record(stream)
@@ -303,13 +310,13 @@ def main():
         ev[k][3].record(stream)
     torch.cuda.synchronize()
     ver.attn.event_begin = ver.attn.event_end = None
-    t_alone_us = float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(K)]) * 1e3)
+    alone = [ev[k][0].elapsed_time(ev[k][1]) * 1e3 for k in range(K)]
+    t_alone_us = float(np.mean(alone))
     t_call_us = float(np.mean([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)]) * 1e3)
 
     # The same attention alone and the same steps over a paged KV cache:
     # 64-token pages in a seeded random order, read through the block table.
-    from paper_2505_17074_amd.batch import PagedKV
-    pk = PagedKV(batch, 64, seed=args.seed)
+    pk = PagedKV(batch, 64, seed=seed)
     pver = Verifier(batch, attn=pk.attn_args())
     for _ in range(Wm):
         pver.run("verify", stream)
@@ -333,7 +340,6 @@ def main():
     # re-reads the same target logits, which the K/V stream (non-temporal
     # loads) leaves in the 256 MB Infinity Cache: the timed loop above is the
     # warm, steady state.
-    flush = CacheFlush(dev)
     KF = min(K, 50)
     for k in range(KF):
         flush()
@@ -354,7 +360,8 @@ def main():
         ver.acc.event_begin, ver.acc.event_end = ev[k][2].cuda_event, ev[k][3].cuda_event
         ver.run("accept", stream)
     torch.cuda.synchronize()
-    t_acc_us = float(np.mean([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)]) * 1e3)
+    acc_cold = [ev[k][2].elapsed_time(ev[k][3]) * 1e3 for k in range(K)]
+    t_acc_us = float(np.mean(acc_cold))
     for k in range(K):
         ver.run("attn", stream)
         ver.acc.event_begin, ver.acc.event_end = ev[k][2].cuda_event, ev[k][3].cuda_event
@@ -382,57 +389,46 @@ def main():
     torch.cuda.synchronize()
     ver.acc.event_begin = ver.acc.event_end = ver.acc.event_mid = None
     t_rows_us = float(np.mean([ev[k][2].elapsed_time(ev[k][4]) for k in range(K)]) * 1e3)
-    del flush
+
+    # the outputs of the last (cold) step stand for every step: same inputs
+    ver.run("verify", stream)
+    res = ver.results()
     logit_bytes = int(work["Nq"]) * pool.vocab * (2 if pool.logit_dtype == W.BF16 else 4)
     achieved = work["attn_bytes"] / (t_attn_us * 1e-6) / 1e9
-    traffic = measured_traffic(args.workload)
     # tokens a step emits: the accepted drafts plus the final token, per request
-    # (the same inputs every step, so the last step's outputs stand for all)
-    emitted = int(batch.accepted_len.to(torch.int64).sum().item()) + pool.batch
-    acc_read = W.accept_bytes_read(pool, batch.accepted_node.cpu().numpy())
-    # the device's stream ceilings last: their 20 ms of full-rate reads and
-    # copies leave the steps that follow them several percent slower
-    read_ceiling, copy_rate = stream_ceilings_gbs(dev)
-
-    line = {
-        "metric": METRIC,
+    emitted = int(res["accepted_len"].astype(np.int64).sum()) + pool.batch
+    acc_read = W.accept_bytes_read(pool, res["accepted_node"])
+    fig = {
         "value": work["Nq"] / (ms * 1e-3),
-        "unit": "verified tokens/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": Wm,
         "ms_per_step": ms,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16" if pool.qkv_dtype == W.BF16 else "f32",
-        "data": "synthetic",
         "config": {"workload": cfg.name, "requests": pool.batch, "verify_tokens": work["Nq"],
                    "kv_tokens": work["Nkv"], "q_heads": pool.num_q_heads, "kv_heads": pool.num_kv_heads,
                    "head_dim": pool.head_dim, "vocab": pool.vocab, "logits": pool.logit_dtype,
-                   "tree_nodes": 0 if pool.tree_parent is None else len(pool.tree_parent), "seed": args.seed},
-        "roofline": {"bound": "hbm", "kernel": "attn_split_mfma", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                   "tree_nodes": 0 if pool.tree_parent is None else len(pool.tree_parent), "seed": seed},
+        "dtype": "bf16" if pool.qkv_dtype == W.BF16 else "f32",
+        # the attention row of the path: the split-KV kernel and the split
+        # combine, timed together by the library's events on their stream
+        "roofline": {"bound": "hbm", "kernel": "attn_split_mfma + attn_combine", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(cfg.name),
                      "algorithmic_bytes": work["attn_bytes"], "kernel_us": t_attn_us,
                      "kernel_us_p10": pct(attn_samples, 10), "kernel_us_p90": pct(attn_samples, 90),
                      "kernel_us_alone": t_alone_us,
+                     "kernel_us_alone_p10": pct(alone, 10), "kernel_us_alone_p90": pct(alone, 90),
                      "frac_alone": work["attn_bytes"] / (t_alone_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
-                     # the whole spec_verify_attn call alone: split + combine, with their launch gaps
+                     # the whole spec_verify_attn call alone, with its launch gaps
                      "call_us_alone": t_call_us,
-                     # the same kernel over a paged KV cache (64-token pages, random order)
+                     "frac_call_alone": work["attn_bytes"] / (t_call_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                     # the same kernels over a paged KV cache (64-token pages, random order)
                      "paged": {"page_tokens": 64, "kernel_us_alone": t_paged_us,
                                "frac_alone": work["attn_bytes"] / (t_paged_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
                                "ms_per_step": ms_paged},
-                     "frac_call_alone": work["attn_bytes"] / (t_call_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
-                     "mfma_util": work["attn_flops"] / (t_attn_us * 1e-6) / MFMA_BF16_PEAK,
-                     "stream_read_GBs": read_ceiling, "frac_of_stream_read": achieved / read_ceiling,
-                     "stream_copy_GBs": copy_rate},
+                     "mfma_util": work["attn_flops"] / (t_attn_us * 1e-6) / MFMA_BF16_PEAK},
         "accepted_plus_bonus_tokens_per_s": emitted / (ms * 1e-3),
-        "cache": "value and ms_per_step: back-to-back steps on the same inputs (warm: the target logits "
-                 "stay in the Infinity Cache); cold: each step after a cache flush",
         "cold": {"steps": KF, "step_us_median": float(np.median(cold)), "step_us_p10": pct(cold, 10),
                  "step_us_p90": pct(cold, 90), "verified_tokens_per_s": work["Nq"] / (float(np.median(cold)) * 1e-6)},
-        "accept": {"kernels_us": t_acc_us, "kernels_us_warm": t_acc_warm_us,
+        "accept": {"kernels_us": t_acc_us, "kernels_us_p10": pct(acc_cold, 10),
+                   "kernels_us_p90": pct(acc_cold, 90), "kernels_us_warm": t_acc_warm_us,
                    "kernels_us_sequential_tree": t_acc_seq_us,
                    "algorithmic_bytes_upper": work["accept_bytes"],
                    "achieved_GBs": work["accept_bytes"] / (t_acc_us * 1e-6) / 1e9,
@@ -445,10 +441,101 @@ def main():
                    "rowstats_us": t_rows_us, "rowstats_bytes": logit_bytes,
                    "rowstats_frac": logit_bytes / (t_rows_us * 1e-6) / 1e9 / HBM_PEAK_GBS},
     }
+    del ver, batch
+    torch.cuda.empty_cache()
+    return fig, pool, res
+
+
+def oracle_check(pool, res) -> dict:
+    """The oracle against this step's GPU outputs (every request): accepted
+    lengths, nodes and next tokens bit-exact except near ties (counted), and
+    the attention's worst row-relative error over every output row."""
+    import numpy as np
+    import oracle
+    acc = oracle.verify_accept(pool.target_logits, pool.draft_probs, pool.draft_tokens, pool.uniforms, pool.n_q,
+                               dtype=pool.logit_dtype, tree_parent=pool.tree_parent)
+    ties = acc["near_tie"]
+    same = np.ones(pool.batch, bool)
+    for key in ("accepted_len", "next_token", "accepted_node"):
+        same &= np.asarray(res[key], np.int64) == acc[key]
+    worst = 0.0
+    q0, kv0 = pool.q_start, pool.kv_start
+    for i in range(pool.batch):
+        n, c = int(pool.n_q[i]), int(pool.ctx_len[i])
+        ref = oracle.verify_attention(pool.q[q0[i]:q0[i] + n], pool.k[kv0[i]:kv0[i + 1]], pool.v[kv0[i]:kv0[i + 1]],
+                                      [c], [n], pool.num_kv_heads, dtype=pool.qkv_dtype,
+                                      tree_parent=pool.tree_parent)
+        got = res["out"][q0[i]:q0[i] + n].astype(np.float64)
+        worst = max(worst, float((np.abs(got - ref).max(-1) / np.abs(ref).max(-1)).max()))
+    return {"requests": pool.batch, "near_ties": int(ties.sum()),
+            "accept_mismatches_outside_ties": int((~same & ~ties).sum()),
+            "accept_mismatches_at_ties": int((~same & ties).sum()),
+            "attention_worst_row_rel_err": worst, "attention_tolerance": 2e-3}
+
+
+def main():
+    args = parse()
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); multi-GPU sharding of the verify step is "
+              "described in the design notes but not built", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    flush = CacheFlush(dev)
+    names = [args.workload] + ([] if args.only else [n for n in OTHERS + (HEADLINE,) if n != args.workload])
+    figs, checks, head_pool = {}, {}, None
+    for name in names:
+        fig, pool, res = measure_workload(name, args.seed, args.steps, args.warmup, dev, flush)
+        figs[name] = fig
+        if not args.no_cpu:
+            # the cpu_baseline leg: the oracle's verdict on this step's outputs
+            checks[name] = oracle_check(pool, res)
+        if name == args.workload:
+            head_pool = pool
+        del pool, res
+    del flush
+    head = figs[args.workload]
+    # the device's stream ceilings last: their 20 ms of full-rate reads and
+    # copies leave the steps that follow them several percent slower
+    read_ceiling, copy_rate = stream_ceilings_gbs(dev)
+    for f in figs.values():
+        f["roofline"]["stream_read_GBs"] = read_ceiling
+        f["roofline"]["frac_of_stream_read"] = f["roofline"]["achieved"] / read_ceiling
+        f["roofline"]["stream_copy_GBs"] = copy_rate
+
+    line = {
+        "metric": METRIC,
+        "value": head["value"],
+        "unit": "verified tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": head["dtype"],
+        "data": "synthetic",
+        "config": head["config"],
+        "roofline": head["roofline"],
+        "accepted_plus_bonus_tokens_per_s": head["accepted_plus_bonus_tokens_per_s"],
+        "cache": "value and ms_per_step: back-to-back steps on the same inputs (warm: the target logits "
+                 "stay in the Infinity Cache); cold: each step after a cache flush",
+        "cold": head["cold"],
+        "accept": head["accept"],
+        # the other workloads, measured the same way in the same run
+        "workloads": {n: f for n, f in figs.items() if n != args.workload},
+    }
     if not args.no_sched:
         line["scheduler"] = scheduler_closed_loop(dev, args.seed)
     if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(pool, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(head_pool, args.cpu_seconds)
+        line["cpu_baseline"]["oracle_check"] = checks
         if not args.no_sched:
             line["cpu_baseline"]["scheduler_oracle_decision_us"] = scheduler_oracle_decision_us(dev, args.seed)
     print(json.dumps(line), flush=True)

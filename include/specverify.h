@@ -165,7 +165,9 @@ typedef struct spec_attn_args {
   float* out;
   int32_t split_kv;
   /* Optional profiling: hipEvent_t handles recorded on `stream` right before
-   * and right after the split-KV attention kernel (NULL = not recorded). */
+   * the split-KV attention kernel and right after the last attention kernel
+   * (the split combine when some request is split, else the split-KV kernel
+   * itself) (NULL = not recorded). */
   void* event_begin;
   void* event_end;
   /* Paged KV cache (above); block_table NULL = the packed layout. */

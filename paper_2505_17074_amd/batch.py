@@ -93,6 +93,12 @@ class Verifier:
     sleeping wait, so the host never wakes late).  A slot's last use is
     `ring` >= `event_every` calls back, so it is always covered by then.
     Calls may be issued back to back without a device sync.
+
+    Every call uses the one device workspace (split partials, acceptance
+    statistics, tickets), so calls are serialised: before a call on a stream
+    other than the previous call's, that stream waits on an event recorded
+    on the previous call's stream after that call.  Calls that should run
+    concurrently need Verifiers of their own.
     """
 
     def __init__(self, batch: DeviceBatch, split_kv: int = 0, ring: int = 32, event_every: int = 8,
@@ -115,6 +121,17 @@ class Verifier:
         self._pending = []                 # slots used since the last event
         self._pending_stream = None
         self._i = 0                        # calls issued
+        self._last_stream = None           # stream of the previous call (workspace owner)
+
+    def _order(self, stream):
+        """Make `stream` wait for the previous call when that call ran on
+        another stream: the two share the workspace."""
+        last = self._last_stream
+        if last is not None and stream != last:
+            ev = torch.cuda.Event()
+            ev.record(last)
+            stream.wait_event(ev)
+        self._last_stream = stream
 
     def _cover(self):
         # a new event each time: one recorded again later, perhaps on another
@@ -147,6 +164,7 @@ class Verifier:
     def run(self, which: str = "verify", stream: Optional[torch.cuda.Stream] = None) -> None:
         stream = stream or torch.cuda.current_stream(self.batch.device)
         s = self._slot(stream)
+        self._order(stream)
         stg = self._staging[s].data_ptr()
         h = stream.cuda_stream
         try:

@@ -545,8 +545,8 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     if (attn->event_begin && hipEventRecord(static_cast<hipEvent_t>(attn->event_begin), st) != hipSuccess)
       return false;
     if (sv::launch_attention(a, attn->dtype == SPEC_BF16, P.nr_max, st) != hipSuccess) return false;
-    if (attn->event_end && hipEventRecord(static_cast<hipEvent_t>(attn->event_end), st) != hipSuccess) return false;
     if (P.parts > 0 && sv::launch_combine(a, st) != hipSuccess) return false;
+    if (attn->event_end && hipEventRecord(static_cast<hipEvent_t>(attn->event_end), st) != hipSuccess) return false;
     return true;
   };
 

@@ -11,6 +11,8 @@ Tolerances:
 from __future__ import annotations
 
 import dataclasses
+import functools
+import zlib
 
 import numpy as np
 
@@ -18,6 +20,28 @@ from oracle import verify_accept, verify_attention
 from paper_2505_17074_amd import workload as W
 
 ATTN_RTOL = 2e-3
+
+
+def case_seed(name: str) -> int:
+    """A fixed seed per named case (CRC-32 of the name, so the same inputs on
+    every run and every machine; Python's str hash is salted per process)."""
+    return zlib.crc32(name.encode()) % 1000
+
+
+def max_near_ties(batch: int) -> int:
+    """Upper bound on the requests a case may excuse as near ties.  The bands
+    (1e-5 in u for a test, 2e-7 in probability mass for the final sample) are
+    expected to catch about 1e-4 of the requests on these workloads and at
+    most 2 of any full-size workload's requests at seeds 0-2; a change that
+    widened the excused set would exceed the bound."""
+    return max(2, int(1e-3 * batch))
+
+
+@functools.lru_cache(maxsize=None)
+def full_pool(idx: int, seed: int = 0) -> W.Pool:
+    """A full-size workload, drawn once per process and shared by the tests
+    that need it (callers must not modify it)."""
+    return W.make_pool(W.CONFIGS[idx], seed)
 
 
 def oracle_attention_rows(pool: W.Pool, reqs) -> dict:
@@ -48,7 +72,9 @@ def oracle_accept(pool: W.Pool, reqs=None) -> dict:
 
 
 def compare_accept(gpu: dict, ref: dict, pool: W.Pool, reqs=None):
-    """Returns (requests that mismatch outside near ties, number of near ties)."""
+    """Returns (requests that mismatch outside near ties, number of near ties).
+    Callers assert that the first is empty and the second at most
+    max_near_ties(batch)."""
     reqs = range(pool.batch) if reqs is None else reqs
     max_len = pool.draft_len if pool.tree_parent is None else np.full(pool.batch, int(pool.draft_len.max()))
     bad, ties = [], 0
@@ -114,3 +140,40 @@ def custom_pool(ctx, k=None, tree_parent=None, Hq=8, Hkv=2, d=128, V=1000, qkv=W
         klen = np.full(B, int(depth.max()), np.int32)
     return W.Pool(dataclasses.replace(cfg, batch=B), seed, ctx, klen, par, np.full(B, sigma), Hq, Hkv, d, qkv,
                   logit, V, q, kk, vv, tl, probs, np.asarray(toks, np.int32), uni)
+
+
+def hand_packed_case():
+    """Two requests packed by hand, with outputs worked by hand (Eq. (1), the
+    residual resample of Sec. 2.2, the extra token of Sec. 4.3).
+
+    Vocabulary 4.  Request 0 drafts k = 2 tokens (target rows 0-2, draft rows
+    0-1, tokens at 0-1, uniforms at 0-2); request 1 drafts k = 1 (target rows
+    3-4, draft row 2, token at q0 - i = 3 - 1 = 2, uniforms at 3-4).  Target
+    logits are log p of the dyadic rows below, so each softmax is p to
+    within fp32 rounding of the logarithms (~1e-7, far from every boundary).
+
+    Request 0: draft 1 is token 1, p0(1) = 1/4, q0(1) = 1/2, u = 1/4:
+      u q = 1/8 < 1/4, accepted.  Draft 2 is token 0, p1(0) = 1/4,
+      q1(0) = 1/2, u = 3/4: u q = 3/8 >= 1/4, rejected, so a = 1.  Residual
+      max(0, p1 - q1) = (0, 0, 1/8, 1/8), total 1/4; final uniform 5/8 puts
+      the target at 5/32; cumulative (0, 0, 1/8, 1/4) first exceeds it at
+      token 3.
+    Request 1: draft 1 is token 0, p3(0) = 1/16, q2(0) = 1/4, u = 1/2:
+      u q = 1/8 >= 1/16, rejected, a = 0.  Residual max(0, p3 - q2) =
+      (0, 0, 1/8, 1/4), total 3/8; final uniform 1/5 puts the target at
+      3/40; cumulative (0, 0, 1/8, 3/8) first exceeds it at token 2.
+    """
+    p = np.array([[1 / 2, 1 / 4, 1 / 8, 1 / 8],      # request 0, verify position 0
+                  [1 / 4, 1 / 4, 1 / 4, 1 / 4],      # request 0, position 1
+                  [1 / 8, 1 / 8, 1 / 4, 1 / 2],      # request 0, position 2 (extra token row)
+                  [1 / 16, 1 / 16, 3 / 8, 1 / 2],    # request 1, position 0
+                  [1 / 8, 3 / 8, 1 / 4, 1 / 4]])     # request 1, position 1 (extra token row)
+    q = np.array([[1 / 4, 1 / 2, 1 / 8, 1 / 8],      # request 0, draft row 0
+                  [1 / 2, 1 / 4, 1 / 8, 1 / 8],      # request 0, draft row 1
+                  [1 / 4, 1 / 4, 1 / 4, 1 / 4]], np.float32)   # request 1, draft row 0
+    inputs = dict(target_logits=np.log(p).astype(np.float32), draft_probs=q,
+                  draft_tokens=np.array([1, 0, 0], np.int32),
+                  uniforms=np.array([0.25, 0.75, 0.625, 0.5, 0.2], np.float32),
+                  ctx=np.array([5, 9], np.int32), draft_len=np.array([2, 1], np.int32))
+    expect = dict(accepted_len=[1, 0], next_token=[3, 2])
+    return inputs, expect

@@ -42,6 +42,7 @@ class _Ring(batch.Verifier):
         self._pending = []
         self._pending_stream = None
         self._i = 0
+        self._last_stream = None
 
 
 @pytest.mark.parametrize("ring,every", [(32, 8), (8, 8), (9, 4), (4, 1), (64, 8)])
@@ -71,3 +72,38 @@ def test_every_reuse_waits_on_a_covering_event(monkeypatch, ring, every, streams
 def test_ring_shorter_than_event_period_is_refused():
     with pytest.raises(ValueError):
         batch.Verifier.__init__(object.__new__(batch.Verifier), None, ring=4, event_every=8)
+
+
+class _Stream:
+    """Stand-in stream: records the calls issued on it and the events it waits on."""
+
+    def __init__(self, name):
+        self.name = name
+        self.waits = []
+
+    def wait_event(self, ev):
+        self.waits.append(ev)
+
+
+def test_calls_on_another_stream_wait_for_the_previous_call(monkeypatch):
+    """The workspace is shared by every call: a call on a stream other than
+    the previous call's must be preceded, on its own stream, by a wait on an
+    event recorded on the previous call's stream after that call."""
+    monkeypatch.setattr(batch, "torch", _FakeTorch)
+    _Ev.last_on = {}
+    rng = random.Random(7)
+    streams = [_Stream(n) for n in "abc"]
+    v = _Ring(8, 4)
+    prev = None
+    for i in range(2000):
+        st = rng.choice(streams)
+        n_waits = len(st.waits)
+        v._order(st)
+        if prev is not None and st is not prev:
+            assert len(st.waits) == n_waits + 1, i
+            ev = st.waits[-1]
+            assert ev.stream is prev and ev.after == _Ev.last_on[prev] == i - 1, i
+        else:
+            assert len(st.waits) == n_waits, i           # same stream: in order already
+        _Ev.last_on[st] = i
+        prev = st

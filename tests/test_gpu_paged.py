@@ -52,8 +52,9 @@ CASES = [
 @pytest.mark.parametrize("page_tokens", [32, 64, 256])
 @pytest.mark.parametrize("name,kw", CASES, ids=[c[0] for c in CASES])
 def test_paged_equals_packed_bitwise(gpu_lib, name, kw, page_tokens):
-    print(f"[case] paged {name} P={page_tokens}", flush=True)
-    pool = U.custom_pool(**kw, seed=hash(name) % 1000)
+    seed = U.case_seed(name)
+    print(f"[case] paged {name} P={page_tokens} seed {seed}", flush=True)
+    pool = U.custom_pool(**kw, seed=seed)
     ref, got, _ = _run(pool, page_tokens)
     assert np.array_equal(got["out"].view(np.uint32), ref["out"].view(np.uint32)), name
     for key in ("accepted_len", "next_token", "accepted_node"):
@@ -89,8 +90,8 @@ def test_paged_against_the_oracle(gpu_lib):
 @pytest.mark.parametrize("idx,page_tokens", [(1, 32), (3, 64), (4, 128)])
 def test_paged_full_size_bitwise(gpu_lib, idx, page_tokens):
     cfg = W.CONFIGS[idx]
-    print(f"[case] paged {cfg.name} full size P={page_tokens}", flush=True)
-    pool = W.make_pool(cfg, 0)
+    print(f"[case] paged {cfg.name} full size P={page_tokens}, seed 0", flush=True)
+    pool = U.full_pool(idx)
     ref, got, _ = _run(pool, page_tokens, which="attn")
     assert np.array_equal(got["out"].view(np.uint32), ref["out"].view(np.uint32)), cfg.name
     torch.cuda.empty_cache()

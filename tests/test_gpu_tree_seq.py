@@ -33,6 +33,7 @@ def _check(pool, tag):
     print(f"{tag} B={pool.batch} mean_depth={res['accepted_len'].mean():.3f} near_ties={ties} mismatches={bad}",
           flush=True)
     assert not bad, (tag, bad)
+    assert ties <= U.max_near_ties(pool.batch), (tag, ties)
     return res, ref
 
 
@@ -43,8 +44,8 @@ def test_tree_workload_reduced(gpu_lib, seed):
 
 
 def test_tree_workload_full_size(gpu_lib):
-    print("[case] sequential tree15 full size", flush=True)
-    res, ref = _check(W.make_pool(W.CONFIGS[4], 0), "tree15/full")
+    print("[case] sequential tree15 full size, seed 0", flush=True)
+    res, ref = _check(U.full_pool(4), "tree15/full")
     # the rule reaches the leaves as well as stopping at the root
     assert res["accepted_len"].max() == 3 and res["accepted_len"].min() == 0
 
@@ -55,8 +56,9 @@ def test_tree_workload_full_size(gpu_lib):
     ("vocab_tail", dict(ctx=[5, 6], tree_parent=[-1, 0, 0, 1, 1], V=4100, sigma=2.5)),
 ], ids=["nonbinary", "wide_root_bf16", "vocab_tail"])
 def test_irregular_trees(gpu_lib, name, kw):
-    print(f"[case] sequential {name}", flush=True)
-    _check(U.custom_pool(**kw, seed=hash(name) % 1000), name)
+    seed = U.case_seed(name)
+    print(f"[case] sequential {name} seed {seed}", flush=True)
+    _check(U.custom_pool(**kw, seed=seed), name)
 
 
 def _cells(breaks):

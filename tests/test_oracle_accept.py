@@ -205,6 +205,19 @@ def test_accepted_length_bounds_random_batches():
         assert 0 <= r["next_token"] < 16
 
 
+def test_batch_packing_by_hand():
+    """The packed batch layout (target rows and uniforms at q0_i, draft tokens
+    at q0_i - i, draft rows at d0_i) against a two-request case worked by
+    hand: a swapped or shifted index changes an output."""
+    from parity_util import hand_packed_case
+    inp, expect = hand_packed_case()
+    r = verify_accept(inp["target_logits"], inp["draft_probs"], inp["draft_tokens"], inp["uniforms"],
+                      inp["draft_len"] + 1)
+    assert r["accepted_len"].tolist() == expect["accepted_len"]
+    assert r["next_token"].tolist() == expect["next_token"]
+    assert not r["near_tie"].any()
+
+
 # ------------------------------------------------------------------- trees
 def test_path_tree_equals_chain_batch():
     rng = np.random.default_rng(3)
