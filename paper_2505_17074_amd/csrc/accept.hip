@@ -2,7 +2,8 @@
 //
 // Two launches, each streaming what it needs once:
 //   acc_rowstats       target-logit rows in 4096-entry chunks: chunk max and
-//                      chunk sum of exp(l - max)              grid Nq x nch
+//                      chunk sum of exp(l - max), 32 KB of a row per
+//                      work-group                    grid Nq x ceil(nch / SUB)
 //                      (independent tree rule: only the rows of nodes with
 //                      children, grid B x inner nodes x nch)
 //   acc_decide_select  per (request, chunk): fold the chunk stats of the
@@ -19,7 +20,7 @@
 //                      u * total, scans inside it and emits the smallest
 //                      token id whose cumulative weight exceeds the target
 //                                                            grid B x nch
-// exp(l - max) is evaluated per entry in fp32 (expf, ~1 ulp), but every sum
+// exp(l - max) is evaluated per entry in fp32 (exp_rel, ~1 ulp), but every sum
 // -- the softmax normaliser Z, chunk masses, prefixes and the in-chunk scan --
 // is accumulated in fp64, and p = e / Z and the residual are formed in fp64.
 // The sampled token then follows the exact inverse CDF except where u * S
@@ -27,6 +28,18 @@
 #include <algorithm>
 
 #include "sv_internal.h"
+
+// Sub-chunks (4096 entries) per row-statistics work-group, by logit dtype.
+#ifndef SV_RS_SUB_F32
+#define SV_RS_SUB_F32 1
+#endif
+#ifndef SV_RS_SUB_BF16
+#define SV_RS_SUB_BF16 1
+#endif
+// Cache policy of the row-statistics loads: 1 = non-temporal hint.
+#ifndef SV_RS_NT
+#define SV_RS_NT 0
+#endif
 
 namespace sv {
 namespace {
@@ -77,6 +90,33 @@ __device__ __forceinline__ void load_vec(const T* row, int v, int V, float pad, 
   }
 }
 
+// load_vec with the row-statistics kernel's cache policy.
+template <typename T>
+__device__ __forceinline__ void load_vec_rs(const T* row, int v, int V, float pad, float* out) {
+  if constexpr (SV_RS_NT) {
+    constexpr int VW = 16 / sizeof(T);
+    if (v + VW <= V) {
+      typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+      const u4v u = __builtin_nontemporal_load(reinterpret_cast<const u4v*>(row + v));
+      if constexpr (sizeof(T) == 4) {
+        out[0] = __uint_as_float(u.x);
+        out[1] = __uint_as_float(u.y);
+        out[2] = __uint_as_float(u.z);
+        out[3] = __uint_as_float(u.w);
+      } else {
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          out[2 * k] = __uint_as_float(w[k] << 16);
+          out[2 * k + 1] = __uint_as_float(w[k] & 0xffff0000u);
+        }
+      }
+      return;
+    }
+  }
+  load_vec(row, v, V, pad, out);
+}
+
 // This thread's 16 entries of chunk `base`, interleaved across the block so
 // every vector load instruction is fully coalesced (order-free reductions).
 template <typename T>
@@ -95,11 +135,31 @@ __device__ __forceinline__ void load16_contiguous(const T* row, int base, int V,
   for (int j = 0; j < 16 / VW; ++j) load_vec(row, base + 16 * threadIdx.x + j * VW, V, pad, x + j * VW);
 }
 
+// exp(x - m) for x <= m (a logit against a maximum): the hardware base-2
+// exponential of (x - m) log2 e.  Its error is about an ulp of the result
+// plus the roundings of x - m and of the product, the same order as the
+// library expf, in three instructions instead of a dozen.  Every kernel
+// below evaluates exp(l - m) through this one function, so a statistic and
+// the entries it summarises are always computed alike.
+__device__ __forceinline__ float exp_rel(float x, float m) {
+  return __builtin_amdgcn_exp2f((x - m) * 1.4426950408889634f);
+}
+
+template <typename T>
+struct RowGeo {
+  static constexpr int VW = 16 / sizeof(T);                 // entries per 16-byte load
+  static constexpr int LPS = kAccChunk / (kAccThreads * VW);  // loads per thread per sub-chunk
+  static constexpr int SUB = sizeof(T) == 4 ? SV_RS_SUB_F32 : SV_RS_SUB_BF16;   // sub-chunks per work-group
+};
+
 template <typename T>
 __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
-  __shared__ float redf[4];
-  __shared__ double redd[4];
-  const int su = blockIdx.x / p.nch, c = blockIdx.x % p.nch;
+  using RG = RowGeo<T>;
+  constexpr int VW = RG::VW, LPS = RG::LPS, SUB = RG::SUB;
+  __shared__ float redf[SUB][4];
+  __shared__ double redd[SUB][4];
+  const int nwg = (p.nch + SUB - 1) / SUB;                 // work-groups per row
+  const int su = blockIdx.x / nwg, c0 = (blockIdx.x % nwg) * SUB;
   // Under the independent tree rule only the rows of nodes with children:
   // their normalisers enter the tests, while a leaf's row is needed only when
   // that leaf is chosen, and the decision kernel then takes its statistics.
@@ -116,22 +176,54 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
   uint4 rq_half;
   const bool copier = blockIdx.x < p.B && threadIdx.x < 2;
   if (copier) rq_half = reinterpret_cast<const uint4*>(p.reqs_src + blockIdx.x)[threadIdx.x];
-  float x[16];
-  if (row >= 0) load16_coalesced(lp, c * kAccChunk, p.V, -INFINITY, x);
+  // Sub-chunk c0 + s is loads s*LPS .. s*LPS + LPS-1: thread t holds entries
+  // (c0+s)*4096 + j*256*VW + t*VW + e, the decision kernel's layout of a chunk,
+  // so both kernels reduce a chunk in the same order (bit-identical statistics).
+  float x[SUB][LPS * VW];
+  if (row >= 0) {
+#pragma unroll
+    for (int sc = 0; sc < SUB; ++sc)
+#pragma unroll
+      for (int j = 0; j < LPS; ++j)
+        load_vec_rs(lp, (c0 + sc) * kAccChunk + j * kAccThreads * VW + threadIdx.x * VW, p.V, -INFINITY,
+                    x[sc] + j * VW);
+  }
   if (copier) {
     reinterpret_cast<uint4*>(p.reqs + blockIdx.x)[threadIdx.x] = rq_half;
     if (threadIdx.x == 0) p.tickets[blockIdx.x] = 0;
   }
   if (row < 0) return;              // uniform: a work-group kept for the copy only
-  float m = -INFINITY;
+  const int wv = threadIdx.x >> 6;
+  float m[SUB];
 #pragma unroll
-  for (int k = 0; k < 16; ++k) m = fmaxf(m, x[k]);
-  m = block_max(m, redf);
-  double s = 0.0;
+  for (int sc = 0; sc < SUB; ++sc) {
+    m[sc] = -INFINITY;
 #pragma unroll
-  for (int k = 0; k < 16; ++k) s += (double)expf(x[k] - m);
-  s = block_sum(s, redd);
-  if (threadIdx.x == 0) p.rowstats[(int64_t)row * p.nch + c] = ChunkStat{s, m, 0.f};
+    for (int k = 0; k < LPS * VW; ++k) m[sc] = fmaxf(m[sc], x[sc][k]);
+    for (int o = 32; o >= 1; o >>= 1) m[sc] = fmaxf(m[sc], __shfl_xor(m[sc], o));
+  }
+  if ((threadIdx.x & 63) == 0)
+#pragma unroll
+    for (int sc = 0; sc < SUB; ++sc) redf[sc][wv] = m[sc];
+  __syncthreads();
+  double sm[SUB];
+#pragma unroll
+  for (int sc = 0; sc < SUB; ++sc) {
+    m[sc] = fmaxf(fmaxf(redf[sc][0], redf[sc][1]), fmaxf(redf[sc][2], redf[sc][3]));
+    sm[sc] = 0.0;
+#pragma unroll
+    for (int k = 0; k < LPS * VW; ++k) sm[sc] += (double)exp_rel(x[sc][k], m[sc]);
+    for (int o = 32; o >= 1; o >>= 1) sm[sc] += __shfl_xor(sm[sc], o);
+  }
+  if ((threadIdx.x & 63) == 0)
+#pragma unroll
+    for (int sc = 0; sc < SUB; ++sc) redd[sc][wv] = sm[sc];
+  __syncthreads();
+  if (threadIdx.x < SUB) {
+    const int sc = threadIdx.x;
+    const double tot = (redd[sc][0] + redd[sc][1]) + (redd[sc][2] + redd[sc][3]);
+    if (c0 + sc < p.nch) p.rowstats[(int64_t)row * p.nch + c0 + sc] = ChunkStat{tot, m[sc], 0.f};
+  }
 }
 
 __device__ __forceinline__ int node_parent(const AccParams& p, int n) {
@@ -146,7 +238,7 @@ __device__ __forceinline__ int node_qrank(const AccParams& p, int n, int N) {
 
 // Final-sample weight of one entry: residual max(0, p - q) or p itself.
 __device__ __forceinline__ double final_weight(float l, float q, float M, double invZ, bool residual) {
-  const double pv = (double)expf(l - M) * invZ;
+  const double pv = (double)exp_rel(l, M) * invZ;
   return residual ? fmax(0.0, pv - (double)q) : pv;
 }
 
@@ -294,7 +386,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
       for (int k = 0; k < 16; ++k) m = fmaxf(m, x[k]);
       m = block_max(m, redf);
 #pragma unroll
-      for (int k = 0; k < 16; ++k) sm += (double)expf(x[k] - m);
+      for (int k = 0; k < 16; ++k) sm += (double)exp_rel(x[k], m);
       sm = block_sum(sm, redd);
     }
     if (tid == 0) {
@@ -396,7 +488,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   double tsum = 0.0;
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
-    w[k] = residual ? final_weight(x[k], q[k], d.M, invZ, true) : (double)expf(x[k] - mcc);
+    w[k] = residual ? final_weight(x[k], q[k], d.M, invZ, true) : (double)exp_rel(x[k], mcc);
     tsum += w[k];
   }
   // exclusive prefix of the per-thread sums, in thread (= token) order
@@ -535,7 +627,7 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
   double invZ = 1.0;
   // running distribution at a token from its logit l and draft probability q
   auto prun = [&](float l, float q) -> double {
-    double x = (double)expf(l - M) * invZ;
+    double x = (double)exp_rel(l, M) * invZ;
     for (int j = 0; j < k; ++j) x = fmax(0.0, x - (double)q) * s_iS[j];
     return x;
   };
@@ -713,9 +805,15 @@ hipError_t launch_rowstats(const AccParams& p, hipStream_t s) {
   dim3 block(kAccThreads);
   // independent tree rule: the rows of nodes with children (at least B work-groups)
   const int64_t rows = p.tree == 1 ? (int64_t)p.B * p.topo.n_inner : (int64_t)p.Nq;
-  const dim3 grid((unsigned)std::max<int64_t>(rows * p.nch, p.B));
-  if (p.bf16) acc_rowstats<uint16_t><<<grid, block, 0, s>>>(p);
-  else acc_rowstats<float><<<grid, block, 0, s>>>(p);
+  if (p.bf16) {
+    constexpr int SUB = RowGeo<uint16_t>::SUB;
+    const dim3 grid((unsigned)std::max<int64_t>(rows * ((p.nch + SUB - 1) / SUB), p.B));
+    acc_rowstats<uint16_t><<<grid, block, 0, s>>>(p);
+  } else {
+    constexpr int SUB = RowGeo<float>::SUB;
+    const dim3 grid((unsigned)std::max<int64_t>(rows * ((p.nch + SUB - 1) / SUB), p.B));
+    acc_rowstats<float><<<grid, block, 0, s>>>(p);
+  }
   return hipGetLastError();
 }
 
