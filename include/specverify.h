@@ -275,6 +275,32 @@ SPEC_API spec_status_t spec_verify(const spec_requests_t* req,
                           void* host_staging, size_t host_staging_bytes,
                           void* stream);
 
+/*
+ * The whole verify step without any allocation, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, outputs and kernels as
+ * spec_verify, but no workspace or staging arguments: the library uses
+ *   - a static device array of SPEC_NOALLOC_SCRATCH_BYTES in its own code
+ *     object (each GPU it runs on holds one until the process ends) as the
+ *     device workspace, and
+ *   - a static host array of SPEC_NOALLOC_STAGING_BYTES for the plan, copied
+ *     into that scratch with hipMemcpyAsync on `stream` (pageable memory:
+ *     the copy has read the plan when the call returns),
+ * and runs both parts on `stream` one after the other (no side stream).
+ * The call makes no hipMalloc, hipFree, stream or event creation.
+ * SPEC_ERR_WORKSPACE when the step needs more scratch or staging than that
+ * (spec_workspace_bytes gives both sizes).  Every call on a GPU shares that
+ * GPU's scratch, which keeps the last call's contents: calls that overlap on
+ * one GPU (two streams, or two host threads without ordering between their
+ * streams) race and must not be made; calls ordered on one stream are safe.
+ */
+#define SPEC_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+#define SPEC_NOALLOC_STAGING_BYTES ((size_t)1 << 20)
+SPEC_API spec_status_t spec_verify_noalloc(const spec_requests_t* req,
+                                           const spec_attn_args_t* attn,
+                                           const spec_accept_args_t* acc,
+                                           void* stream);
+
 /* Static text for a status code. */
 SPEC_API const char* spec_status_str(spec_status_t status);
 

@@ -17,9 +17,11 @@ SPEC_F32, SPEC_BF16 = 0, 1
 SPEC_TREE_INDEPENDENT, SPEC_TREE_SEQUENTIAL = 0, 1
 SPEC_MAX_DRAFT = 16
 SPEC_MAX_TREE_NODES = 32
+SPEC_NOALLOC_SCRATCH_BYTES = 32 << 20
+SPEC_NOALLOC_STAGING_BYTES = 1 << 20
 
 EXPORTS = ("spec_workspace_bytes", "spec_verify_attn", "spec_accept", "spec_verify",
-           "spec_status_str", "spec_abi_version", "spec_stream_read_probe",
+           "spec_status_str", "spec_abi_version", "spec_stream_read_probe", "spec_verify_noalloc",
            "spec_sched_create", "spec_sched_destroy", "spec_sched_submit", "spec_sched_next",
            "spec_sched_report", "spec_sched_query", "spec_sched_simulate")
 
@@ -157,6 +159,8 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.spec_verify.argtypes = [P(SpecRequests), P(SpecAttnArgs), P(SpecAcceptArgs), C.c_void_p, C.c_size_t,
                                 C.c_void_p, C.c_size_t, C.c_void_p]
     lib.spec_verify.restype = C.c_int
+    lib.spec_verify_noalloc.argtypes = [P(SpecRequests), P(SpecAttnArgs), P(SpecAcceptArgs), C.c_void_p]
+    lib.spec_verify_noalloc.restype = C.c_int
     lib.spec_status_str.argtypes = [C.c_int]
     lib.spec_status_str.restype = C.c_char_p
     lib.spec_abi_version.argtypes = []
@@ -213,6 +217,10 @@ def spec_accept(req, acc, ws: int, ws_bytes: int, staging: int, staging_bytes: i
 
 def spec_verify(req, attn, acc, ws: int, ws_bytes: int, staging: int, staging_bytes: int, stream: int) -> int:
     return load().spec_verify(C.byref(req), _ref(attn), _ref(acc), ws, ws_bytes, staging, staging_bytes, stream)
+
+
+def spec_verify_noalloc(req, attn, acc, stream: int) -> int:
+    return load().spec_verify_noalloc(C.byref(req), _ref(attn), _ref(acc), stream)
 
 
 def spec_abi_version() -> int:

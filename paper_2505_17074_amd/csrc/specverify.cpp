@@ -436,8 +436,19 @@ void write_staging(const Plan& P, void* host) {
   std::memcpy(h + P.off_rowreq, P.row_req.data(), sizeof(int32_t) * P.row_req.size());
 }
 
+// How run() places the work: the normal entry points overlap the two parts
+// on a side stream and take the caller's staging; the no-allocation entry
+// point keeps everything on the caller's stream and stages the plan in
+// library-owned pageable memory, which is always copied.
+struct RunMode {
+  bool overlap = true;
+  bool pageable = false;      // staging known not to be device-mapped
+  std::mutex* staging_mu = nullptr;   // held while the staging is written and the copy enqueued
+};
+
 spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, const spec_accept_args_t* acc,
-                  void* ws, size_t ws_bytes, void* staging, size_t staging_bytes, void* stream) {
+                  void* ws, size_t ws_bytes, void* staging, size_t staging_bytes, void* stream,
+                  const RunMode& mode = RunMode()) {
   Plan P;
   spec_status_t st = build_plan(req, attn, acc, P);
   if (st != SPEC_OK) return st;
@@ -446,17 +457,22 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* d = static_cast<char*>(ws);
-  write_staging(P, staging);
   // The kernels read the plan where it was staged when the staging buffer is
   // device-mapped pinned memory (no upload pass ahead of them); otherwise it
   // is copied into the workspace first.
   const char* pl = d;
-  void* mapped = nullptr;
-  if (hipHostGetDevicePointer(&mapped, staging, 0) == hipSuccess && mapped && aligned16(mapped)) {
-    pl = static_cast<const char*>(mapped);
-  } else {
-    (void)hipGetLastError();   // clear the lookup's error state
-    if (hipMemcpyAsync(d, staging, P.plan_bytes, hipMemcpyHostToDevice, s) != hipSuccess) return SPEC_ERR_HIP;
+  {
+    std::unique_lock<std::mutex> lk;
+    if (mode.staging_mu) lk = std::unique_lock<std::mutex>(*mode.staging_mu);
+    write_staging(P, staging);
+    void* mapped = nullptr;
+    if (!mode.pageable && hipHostGetDevicePointer(&mapped, staging, 0) == hipSuccess && mapped &&
+        aligned16(mapped)) {
+      pl = static_cast<const char*>(mapped);
+    } else {
+      if (!mode.pageable) (void)hipGetLastError();   // clear the lookup's error state
+      if (hipMemcpyAsync(d, staging, P.plan_bytes, hipMemcpyHostToDevice, s) != hipSuccess) return SPEC_ERR_HIP;
+    }
   }
 
   sv::AttnParams a{};
@@ -553,7 +569,7 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
 #ifndef SV_OVERLAP
 #define SV_OVERLAP 1
 #endif
-  if (SV_OVERLAP && attn && acc) {
+  if (SV_OVERLAP && mode.overlap && attn && acc) {
     SideStream* S = side_stream();
     if (!S) return SPEC_ERR_HIP;
     std::lock_guard<std::mutex> lk(S->mu);
@@ -604,6 +620,29 @@ spec_status_t spec_verify(const spec_requests_t* req, const spec_attn_args_t* at
                           void* stream) {
   if (!attn || !acc) return SPEC_ERR_INVALID_ARG;
   return run(req, attn, acc, workspace, workspace_bytes, host_staging, host_staging_bytes, stream);
+}
+
+// The no-allocation variant of spec_verify: the library's static device
+// scratch as the workspace, its static host array as the staging, and no
+// side stream.  Pageable host memory: hipMemcpyAsync has read the plan out
+// of the array before it returns, and the mutex keeps two host threads from
+// writing the array at once.
+spec_status_t spec_verify_noalloc(const spec_requests_t* req, const spec_attn_args_t* attn,
+                                  const spec_accept_args_t* acc, void* stream) {
+  static char host_staging[sv::kNoAllocStagingBytes];
+  static std::mutex staging_mu;
+  if (!attn || !acc) return SPEC_ERR_INVALID_ARG;
+  Plan P;
+  const spec_status_t st = build_plan(req, attn, acc, P);   // argument checks before any HIP call
+  if (st != SPEC_OK) return st;
+  if (P.device_bytes > sv::kNoAllocScratchBytes || P.plan_bytes > sv::kNoAllocStagingBytes) return SPEC_ERR_WORKSPACE;
+  void* scratch = nullptr;
+  if (sv::noalloc_scratch(&scratch) != hipSuccess) return SPEC_ERR_HIP;
+  RunMode mode;
+  mode.overlap = false;
+  mode.pageable = true;
+  mode.staging_mu = &staging_mu;
+  return run(req, attn, acc, scratch, sv::kNoAllocScratchBytes, host_staging, sizeof(host_staging), stream, mode);
 }
 
 const char* spec_status_str(spec_status_t status) {

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/specverify.h"
+
 namespace sv {
 
 constexpr int kMaxNodes = 32;          // verify positions per request (chain k+1 or tree)
@@ -146,5 +148,13 @@ hipError_t launch_decide(const AccParams& p, hipStream_t s);
 // and 4 (draft probability at a draft token not > 0).
 hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_t s);
 hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* out, int blocks, hipStream_t s);
+
+// The no-allocation entry point's device scratch (a static device array of
+// kNoAllocScratchBytes) and its host staging (a static host array of
+// kNoAllocStagingBytes).  noalloc_scratch returns the current device's
+// address of the array, looked up once per device.
+constexpr size_t kNoAllocScratchBytes = SPEC_NOALLOC_SCRATCH_BYTES;
+constexpr size_t kNoAllocStagingBytes = SPEC_NOALLOC_STAGING_BYTES;
+hipError_t noalloc_scratch(void** ptr);
 
 }  // namespace sv

@@ -261,3 +261,23 @@ def test_paged_block_stride_must_hold_every_page(lib):
     # 3000 + 3 rows need 94 pages of 32
     assert _ws(_req(ctx=(3000, 5), k=(2, 1)), _attn(**{**PAGED, "block_stride": 93}), None)[0] == B.SPEC_ERR_INVALID_ARG
     assert _ws(_req(ctx=(3000, 5), k=(2, 1)), _attn(**{**PAGED, "block_stride": 94}), None)[0] == B.SPEC_OK
+
+
+def test_noalloc_checks_before_any_hip_call(lib):
+    """spec_verify_noalloc runs the same argument checks as spec_verify before
+    any HIP call, and refuses a step that needs more than its static scratch
+    (SPEC_ERR_WORKSPACE): both answer on a host without a GPU."""
+    h = 0
+    assert B.spec_verify_noalloc(_req(ctx=(5, -1)), _attn(), _acc(), h) == B.SPEC_ERR_INVALID_ARG
+    assert lib.spec_verify_noalloc(C.byref(_req()), None, C.byref(_acc()), None) == B.SPEC_ERR_INVALID_ARG
+    assert lib.spec_verify_noalloc(C.byref(_req()), C.byref(_attn()), None, None) == B.SPEC_ERR_INVALID_ARG
+    assert B.spec_verify_noalloc(_req(), _attn(head_dim=96), _acc(), h) == B.SPEC_ERR_UNSUPPORTED
+    # 32-key pieces of long contexts: split partials beyond the static scratch
+    big = _req(ctx=(60000, 60000, 60000), k=(16, 16, 16))
+    st, dev, _ = _ws(big, _attn(split_kv=32), _acc())
+    assert st == B.SPEC_OK and dev > B.SPEC_NOALLOC_SCRATCH_BYTES
+    assert B.spec_verify_noalloc(big, _attn(split_kv=32), _acc(), h) == B.SPEC_ERR_WORKSPACE
+    # the header's limits are the binding's
+    text = open(HEADER).read()
+    assert "#define SPEC_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)" in text
+    assert "#define SPEC_NOALLOC_STAGING_BYTES ((size_t)1 << 20)" in text
