@@ -226,10 +226,10 @@ def cpu_baseline(pool, budget_s: float):
         n, c = int(n_q[i]), int(pool.ctx_len[i])
         t0 = time.perf_counter()
         oracle.verify_attention(pool.q[q0[i]:q0[i] + n], pool.k[kv0[i]:kv0[i + 1]], pool.v[kv0[i]:kv0[i + 1]],
-                                [c], [n], pool.num_kv_heads, dtype=pool.qkv_dtype, tree_parent=pool.tree_parent)
+                                [c], [n], pool.num_kv_heads, dtype=pool.qkv_dtype, tree_parent=pool.parents_of(i))
         oracle.verify_accept(pool.target_logits[q0[i]:q0[i] + n], pool.draft_probs[pool.d_start[i]:pool.d_start[i + 1]],
                              pool.draft_tokens[q0[i] - i:q0[i] - i + n - 1], pool.uniforms[q0[i]:q0[i] + n], [n],
-                             dtype=pool.logit_dtype, tree_parent=pool.tree_parent)
+                             dtype=pool.logit_dtype, tree_parent=pool.parents_of(i))
         t_used += time.perf_counter() - t0
         done_tokens += n
         m += 1
@@ -453,7 +453,7 @@ def oracle_check(pool, res) -> dict:
     import numpy as np
     import oracle
     acc = oracle.verify_accept(pool.target_logits, pool.draft_probs, pool.draft_tokens, pool.uniforms, pool.n_q,
-                               dtype=pool.logit_dtype, tree_parent=pool.tree_parent)
+                               dtype=pool.logit_dtype, tree_parent=pool.tree_parent, tree_parents=pool.tree_parents)
     ties = acc["near_tie"]
     same = np.ones(pool.batch, bool)
     for key in ("accepted_len", "next_token", "accepted_node"):
@@ -464,7 +464,7 @@ def oracle_check(pool, res) -> dict:
         n, c = int(pool.n_q[i]), int(pool.ctx_len[i])
         ref = oracle.verify_attention(pool.q[q0[i]:q0[i] + n], pool.k[kv0[i]:kv0[i + 1]], pool.v[kv0[i]:kv0[i + 1]],
                                       [c], [n], pool.num_kv_heads, dtype=pool.qkv_dtype,
-                                      tree_parent=pool.tree_parent)
+                                      tree_parent=pool.parents_of(i))
         got = res["out"][q0[i]:q0[i] + n].astype(np.float64)
         worst = max(worst, float((np.abs(got - ref).max(-1) / np.abs(ref).max(-1)).max()))
     return {"requests": pool.batch, "near_ties": int(ties.sum()),

@@ -71,7 +71,7 @@ extern "C" {
 #define SPEC_API
 #endif
 
-#define SPEC_ABI_VERSION 4
+#define SPEC_ABI_VERSION 5
 #define SPEC_MAX_DRAFT 16        /* chain drafts per request */
 #define SPEC_MAX_TREE_NODES 32   /* token-tree nodes per request, root included */
 
@@ -100,15 +100,24 @@ typedef enum spec_dtype {
  *   draft_len[B]  chain mode: k_i in [0, SPEC_MAX_DRAFT] drafts (k_i = 0 is
  *                 plain decoding: no test, one sample from the target).
  *                 Ignored (may be NULL) in tree mode.
- *   tree_nodes    0 = chain mode.  Otherwise every request verifies the same
- *                 token-tree topology of tree_nodes nodes (1 ..
+ *   tree_nodes    0 = no shared tree.  Otherwise every request verifies the
+ *                 same token-tree topology of tree_nodes nodes (1 ..
  *                 SPEC_MAX_TREE_NODES), node 0 being the last accepted token.
  *   tree_parent   [tree_nodes], BFS order: parent[0] = -1, 0 <= parent[n] < n.
+ *   node_count    NULL, or per-request token trees (tree_nodes must then be
+ *                 0; draft_len is ignored): request i verifies its own tree
+ *                 of node_count[i] nodes (1 .. SPEC_MAX_TREE_NODES), the
+ *                 SpecInfer setup of one speculated tree per request.
+ *   tree_parents  [sum node_count] with node_count: request i's BFS parent
+ *                 array at tree_parents[o_i .. o_i + node_count[i]), o_i the
+ *                 running sum of node_count over requests < i; each array as
+ *                 tree_parent above.
  *
- * Derived counts: n_i = k_i + 1 (chain) or tree_nodes verify positions;
- * Nq = sum n_i;  Nkv = sum (c_i + n_i);  Nd = sum of the number of nodes
- * that have children (k_i for a chain).  Request i's rows of every packed
- * array start at the running sum of the matching count over requests < i.
+ * Derived counts: n_i = k_i + 1 (chain), tree_nodes (shared tree) or
+ * node_count[i] verify positions; Nq = sum n_i;  Nkv = sum (c_i + n_i);
+ * Nd = sum of the number of nodes that have children (k_i for a chain).
+ * Request i's rows of every packed array start at the running sum of the
+ * matching count over requests < i.
  */
 typedef struct spec_requests {
   int32_t num_requests;
@@ -116,6 +125,8 @@ typedef struct spec_requests {
   const int32_t* draft_len;
   int32_t tree_nodes;
   const int32_t* tree_parent;
+  const int32_t* node_count;
+  const int32_t* tree_parents;
 } spec_requests_t;
 
 /*

@@ -197,22 +197,22 @@ def verify_accept(target_logits: np.ndarray, draft_probs: np.ndarray,
                   n_q: Sequence[int], dtype: str = "f32",
                   tree_parent: Optional[Sequence[int]] = None,
                   requests: Optional[Sequence[int]] = None,
-                  tree_rule: str = "independent") -> dict:
+                  tree_rule: str = "independent",
+                  tree_parents: Optional[Sequence[Sequence[int]]] = None) -> dict:
     """Acceptance for a packed batch (layouts as in the C interface).
 
     Request i owns target rows q0_i .. q0_i + n_i - 1 (q0 = running sum of
     n_i), uniforms at the same rows, draft tokens q0_i - i .. q0_i - i + n_i - 2
     (one per non-root node) and draft rows d0_i .. (d0 = running sum of the
-    number of nodes with children: k_i for a chain).  ``requests`` restricts
-    the work to a subset (results for the others are -1).
+    number of nodes with children: k_i for a chain).  A token tree is shared
+    (tree_parent) or given per request (tree_parents[i]).  ``requests``
+    restricts the work to a subset (results for the others are -1).
     """
     n_q = [int(x) for x in n_q]
     B = len(n_q)
-    if tree_parent is not None:
-        has_child = sorted(set(int(x) for x in tree_parent[1:]))
-        n_int = [len(has_child)] * B
-    else:
-        n_int = [n - 1 for n in n_q]
+    pars = [tree_parents[i] if tree_parents is not None else tree_parent for i in range(B)]
+    inner = [None if par is None else sorted(set(int(x) for x in par[1:])) for par in pars]
+    n_int = [n - 1 if inner[i] is None else len(inner[i]) for i, n in enumerate(n_q)]
     q0 = np.concatenate([[0], np.cumsum(n_q)]).astype(np.int64)
     d0 = np.concatenate([[0], np.cumsum(n_int)]).astype(np.int64)
     keys = ("accepted_len", "next_token", "accepted_node")
@@ -226,13 +226,15 @@ def verify_accept(target_logits: np.ndarray, draft_probs: np.ndarray,
         p_rows = np.stack([softmax64(widen(target_logits[q0[i] + j], dtype)) for j in range(n)])
         toks = np.asarray(draft_tokens[q0[i] - i: q0[i] - i + n - 1], dtype=np.int64)
         us = np.asarray(uniforms[q0[i]: q0[i] + n], dtype=np.float64)
-        if tree_parent is None:
+        if pars[i] is None:
             q_rows = widen(draft_probs[d0[i]: d0[i] + n - 1], dtype).reshape(n - 1, target_logits.shape[1])
             r = accept_chain(p_rows, q_rows, toks, us)
         else:
-            q_rows = {node: widen(draft_probs[d0[i] + rnk], dtype) for rnk, node in enumerate(has_child)}
+            if len(pars[i]) != n:
+                raise ValueError("tree size must equal the number of verify nodes")
+            q_rows = {node: widen(draft_probs[d0[i] + rnk], dtype) for rnk, node in enumerate(inner[i])}
             rule = accept_tree_sequential if tree_rule == "sequential" else accept_tree
-            r = rule(p_rows, q_rows, toks, us, tree_parent)
+            r = rule(p_rows, q_rows, toks, us, pars[i])
         for key in keys:
             res[key][i] = r[key]
         res["near_tie"][i] = r["near_tie"]

@@ -17,8 +17,10 @@ query head h and verify node j:
 
 anc*(j) is the set of ancestors of node j together with j itself: {0..j} for
 a chain (causal mask inside the verify block), the root-to-node path for a
-tree.  The verify block's keys and values are the last n_i rows of the
-request's KV rows.  scale defaults to 1/sqrt(d).
+tree.  A token tree is either shared by every request of the batch or given
+per request (each request its own BFS parent array).  The verify block's keys
+and values are the last n_i rows of the request's KV rows.  scale defaults to
+1/sqrt(d).
 """
 from __future__ import annotations
 
@@ -53,12 +55,15 @@ def ancestors_or_self(parent: Sequence[int]) -> list:
 def verify_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
                      ctx_len: Sequence[int], n_q: Sequence[int], num_kv_heads: int,
                      dtype: str = "f32", tree_parent: Optional[Sequence[int]] = None,
-                     scale: Optional[float] = None) -> np.ndarray:
+                     scale: Optional[float] = None,
+                     tree_parents: Optional[Sequence[Sequence[int]]] = None) -> np.ndarray:
     """Verify attention for a packed ragged batch; returns fp64 [Nq, Hq, d].
 
     q: [Nq, Hq, d]; k, v: [Nkv, Hkv, d]; request i owns query rows
     q0_i .. q0_i + n_i - 1 and KV rows kv0_i .. kv0_i + c_i + n_i - 1, with
-    q0 and kv0 the running sums of n_i and c_i + n_i.
+    q0 and kv0 the running sums of n_i and c_i + n_i.  tree_parent: one tree
+    for every request; tree_parents: request i's tree is tree_parents[i]
+    (None for both: chains).
     """
     Q = widen(q, dtype)
     Nq, Hq, d = Q.shape
@@ -70,15 +75,16 @@ def verify_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray,
         scale = 1.0 / np.sqrt(d)
     out = np.zeros((Nq, Hq, d), dtype=np.float64)
     q0 = kv0 = 0
-    for c, n in zip(ctx_len, n_q):
+    for i, (c, n) in enumerate(zip(ctx_len, n_q)):
         c, n = int(c), int(n)
         L = c + n
-        if tree_parent is None:
+        par = tree_parents[i] if tree_parents is not None else tree_parent
+        if par is None:
             anc = [set(range(j + 1)) for j in range(n)]
         else:
-            if len(tree_parent) != n:
+            if len(par) != n:
                 raise ValueError("tree size must equal the number of verify nodes")
-            anc = ancestors_or_self(tree_parent)
+            anc = ancestors_or_self(par)
         # visibility of each key position to each verify node
         mask = np.zeros((n, L), dtype=bool)
         mask[:, :c] = True

@@ -49,6 +49,8 @@ class DeviceBatch:
 
     def requests(self) -> B.SpecRequests:
         p = self.pool
+        if p.tree_parents is not None:
+            return B.make_requests(p.ctx_len, tree_parents=p.tree_parents)
         if p.tree_parent is not None:
             return B.make_requests(p.ctx_len, None, p.tree_parent)
         return B.make_requests(p.ctx_len, p.draft_len)

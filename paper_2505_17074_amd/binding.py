@@ -35,7 +35,9 @@ class SpecRequests(C.Structure):
                 ("ctx_len", C.POINTER(C.c_int32)),
                 ("draft_len", C.POINTER(C.c_int32)),
                 ("tree_nodes", C.c_int32),
-                ("tree_parent", C.POINTER(C.c_int32))]
+                ("tree_parent", C.POINTER(C.c_int32)),
+                ("node_count", C.POINTER(C.c_int32)),
+                ("tree_parents", C.POINTER(C.c_int32))]
 
 
 class SpecAttnArgs(C.Structure):
@@ -231,8 +233,10 @@ def spec_stream_read_probe(src, nbytes, out, blocks, stream):
     return load().spec_stream_read_probe(src, nbytes, out, blocks, stream)
 
 
-def make_requests(ctx_len, draft_len=None, tree_parent=None):
-    """SpecRequests over host int32 arrays; the arrays are kept alive on the struct."""
+def make_requests(ctx_len, draft_len=None, tree_parent=None, tree_parents=None):
+    """SpecRequests over host int32 arrays; the arrays are kept alive on the struct.
+    Chains (draft_len), one shared tree (tree_parent) or a tree per request
+    (tree_parents: one BFS parent array per request)."""
     import numpy as np
     ctx = np.ascontiguousarray(ctx_len, dtype=np.int32)
     r = SpecRequests()
@@ -250,5 +254,11 @@ def make_requests(ctx_len, draft_len=None, tree_parent=None):
         keep.append(par)
     else:
         r.tree_nodes = 0
+    if tree_parents is not None:
+        cnt = np.ascontiguousarray([len(x) for x in tree_parents], dtype=np.int32)
+        cat = np.ascontiguousarray(np.concatenate([np.asarray(x, np.int32) for x in tree_parents]), dtype=np.int32)
+        r.node_count = cnt.ctypes.data_as(C.POINTER(C.c_int32))
+        r.tree_parents = cat.ctypes.data_as(C.POINTER(C.c_int32))
+        keep += [cnt, cat]
     r._keep = keep
     return r

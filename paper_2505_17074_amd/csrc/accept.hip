@@ -165,7 +165,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
   // that leaf is chosen, and the decision kernel then takes its statistics.
   // Every request has the tree's `nodes` rows there, so the row is arithmetic.
   int row = su;
-  if (p.tree == 1) {
+  if (p.tree == 1 && !p.per_req) {
     const int ni = p.topo.n_inner;
     row = (ni > 0 && su < p.B * ni) ? (su / ni) * p.topo.nodes + p.topo.inner[su % ni] : -1;
   }
@@ -192,6 +192,10 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
     reinterpret_cast<uint4*>(p.reqs + blockIdx.x)[threadIdx.x] = rq_half;
     if (threadIdx.x == 0) p.tickets[blockIdx.x] = 0;
   }
+  // per-request trees: the same work-groups copy the node table
+  if (p.per_req && blockIdx.x < p.B)
+    for (int x = blockIdx.x * kAccThreads + threadIdx.x; x < p.nodes_n16; x += p.B * kAccThreads)
+      reinterpret_cast<uint4*>(p.nodes)[x] = reinterpret_cast<const uint4*>(p.nodes_src)[x];
   if (row < 0) return;              // uniform: a work-group kept for the copy only
   const int wv = threadIdx.x >> 6;
   float m[SUB];
@@ -234,6 +238,29 @@ __device__ __forceinline__ int node_depth(const AccParams& p, int n) {
 }
 __device__ __forceinline__ int node_qrank(const AccParams& p, int n, int N) {
   return p.tree ? p.topo.qrank[n] : (n < N - 1 ? n : -1);
+}
+
+// Node n of request rq: its parent, depth, draft-row rank (nodes with
+// children) and its parent's draft-row rank, from the request's node-table
+// entry (per-request trees), the shared tree or the chain.
+struct NodeRec {
+  int par, dep, qr, pq;
+};
+__device__ __forceinline__ NodeRec node_rec(const AccParams& p, const NodeInfo* nodes, const ReqInfo& rq, int n) {
+  NodeRec r;
+  if (p.per_req) {
+    const NodeInfo e = nodes[rq.node0 + n];
+    r.par = e.parent;
+    r.dep = e.depth;
+    r.qr = e.qrank;
+    r.pq = e.pqrank;
+  } else {
+    r.par = node_parent(p, n);
+    r.dep = node_depth(p, n);
+    r.qr = node_qrank(p, n, rq.nq);
+    r.pq = n > 0 ? node_qrank(p, r.par, rq.nq) : -1;
+  }
+  return r;
 }
 
 // Final-sample weight of one entry: residual max(0, p - q) or p itself.
@@ -287,6 +314,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   __shared__ float s_mrow, s_mcc;
   __shared__ int s_chunk;
   __shared__ int s_cand[4], s_last_pos[4];
+  __shared__ int s_par[kMaxNodes], s_dep[kMaxNodes], s_qr[kMaxNodes];
   const int i = blockIdx.x / p.nch, c = blockIdx.x % p.nch;
   const int tid = threadIdx.x, wv = tid >> 6, ln = tid & 63;
   const ReqInfo rq = p.reqs[i];
@@ -301,18 +329,24 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   const bool tester = n >= 1 && n < N;      // lanes of wave 0 only (N <= 32)
   int par = 0;
   float lx = 0.f, qx = 0.f, un = 0.f;
-  if (tester) {
-    par = node_parent(p, n);
-    // an out-of-range id (the caller's contract) is clamped: no read leaves the row
-    const int x = min(max(p.tokens[rq.q0 - i + n - 1], 0), p.V - 1);
-    lx = ld(L, (int64_t)(rq.q0 + par) * p.l_st + x);
-    qx = ld(Q, (int64_t)(rq.d0 + node_qrank(p, par, N)) * p.p_st + x);
-    un = p.uniforms[rq.q0 + n - 1];
+  if (n < N) {
+    const NodeRec nr = node_rec(p, p.nodes, rq, n);
+    s_par[n] = nr.par;
+    s_dep[n] = nr.dep;
+    s_qr[n] = nr.qr;
+    if (tester) {
+      par = nr.par;
+      // an out-of-range id (the caller's contract) is clamped: no read leaves the row
+      const int x = min(max(p.tokens[rq.q0 - i + n - 1], 0), p.V - 1);
+      lx = ld(L, (int64_t)(rq.q0 + par) * p.l_st + x);
+      qx = ld(Q, (int64_t)(rq.d0 + nr.pq) * p.p_st + x);
+      un = p.uniforms[rq.q0 + n - 1];
+    }
   }
 
   // (M, Z) of every row of the request that has chunk statistics
   for (int r = wv; r < N; r += kAccThreads / 64) {
-    if (p.tree == 1 && p.topo.qrank[r] < 0) continue;     // a leaf's row: none yet
+    if (p.tree == 1 && !p.per_req && p.topo.qrank[r] < 0) continue;     // a leaf's row: none yet
     const ChunkStat* st = p.rowstats + (int64_t)(rq.q0 + r) * p.nch;
     float m = -INFINITY;
     for (int k = ln; k < p.nch; k += 64) m = fmaxf(m, st[k].m);
@@ -339,18 +373,18 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
       uint32_t accepted = 1u;   // bit per node
       int best = 0;
       for (int m = 1; m < N; ++m) {
-        const int par = node_parent(p, m);
+        const int par = s_par[m];
         if (((accepted >> par) & 1u) && ((passmask >> m) & 1ull)) {
           accepted |= 1u << m;
-          if (node_depth(p, m) > node_depth(p, best)) best = m;
+          if (s_dep[m] > s_dep[best]) best = m;
         }
       }
-      const int qrank = node_qrank(p, best, N);
+      const int qrank = s_qr[best];
       Decision d;
       d.node = best;
       d.row = rq.q0 + best;
       d.qrow = qrank >= 0 ? rq.d0 + qrank : -1;
-      d.len = node_depth(p, best);
+      d.len = s_dep[best];
       d.M = qrank >= 0 ? s_M[best] : 0.f;      // the residual's normaliser (a node with children)
       d.Z = qrank >= 0 ? s_Z[best] : 1.0;
       d.pad = 0.f;
@@ -361,7 +395,8 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   const Decision d = s_dec;
   const double invZ = 1.0 / d.Z;
   bool residual = d.qrow >= 0;
-  const bool own_stats = !residual && p.tree == 1;   // a leaf's row under the independent tree rule
+  // a leaf's row under the independent rule over a shared tree has no statistics yet
+  const bool own_stats = !residual && p.tree == 1 && !p.per_req;
   const T* Lr = L + (int64_t)d.row * p.l_st;
   const T* Qr = Q + (int64_t)(d.qrow >= 0 ? d.qrow : 0) * p.p_st;
   ChunkStat* rst = p.rowstats + (int64_t)d.row * p.nch;
@@ -586,6 +621,7 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
   __shared__ double s_run, s_target;
   __shared__ int s_pos[NW];
   __shared__ int s_pick;
+  __shared__ int s_par[kMaxNodes], s_dep[kMaxNodes], s_qr[kMaxNodes];
   const int i = blockIdx.x;
   const int tid = threadIdx.x, wv = tid >> 6, ln = tid & 63;
   const ReqInfo rq = p.reqs[i];
@@ -595,13 +631,17 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
 
   // every child's test inputs, which do not depend on the walk: its token,
   // its parent's logit and draft probability there, and its uniform
-  if (tid >= 1 && tid < N) {
-    const int par = node_parent(p, tid);
-    const int x = min(max(p.tokens[rq.q0 - i + tid - 1], 0), p.V - 1);
-    const int qr = node_qrank(p, par, N);
-    s_lx[tid] = ld(L + (int64_t)(rq.q0 + par) * p.l_st, x);
-    s_qx[tid] = qr >= 0 ? ld(Q + (int64_t)(rq.d0 + qr) * p.p_st, x) : 0.f;
-    s_u[tid] = p.uniforms[rq.q0 + tid - 1];
+  if (tid < N) {
+    const NodeRec nr = node_rec(p, p.nodes, rq, tid);
+    s_par[tid] = nr.par;
+    s_dep[tid] = nr.dep;
+    s_qr[tid] = nr.qr;
+    if (tid >= 1) {
+      const int x = min(max(p.tokens[rq.q0 - i + tid - 1], 0), p.V - 1);
+      s_lx[tid] = ld(L + (int64_t)(rq.q0 + nr.par) * p.l_st, x);
+      s_qx[tid] = nr.pq >= 0 ? ld(Q + (int64_t)(rq.d0 + nr.pq) * p.p_st, x) : 0.f;
+      s_u[tid] = p.uniforms[rq.q0 + tid - 1];
+    }
   }
   // (M, Z) of every row of the request, as in the decision kernel
   for (int r = wv; r < N; r += NW) {
@@ -643,13 +683,13 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
     M = s_M[node];
     invZ = 1.0 / s_Z[node];
     Lr = L + (int64_t)(rq.q0 + node) * p.l_st;
-    const int qr = node_qrank(p, node, N);
+    const int qr = s_qr[node];
     has_q = qr >= 0;
     Qr = Q + (int64_t)(rq.d0 + (has_q ? qr : 0)) * p.p_st;
     k = 0;
     int next = -1;
     for (int c = node + 1; c < N && next < 0; ++c) {
-      if (node_parent(p, c) != node) continue;
+      if (s_par[c] != node) continue;
       const float qx = s_qx[c];
       const double px = prun(s_lx[c], qx);
       if ((double)s_u[c] * (double)qx < px) {
@@ -761,7 +801,7 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
     // a target at or past the total (rounding): the last id with positive weight
     if (v < 0)
       for (int w = 0; w < NW; ++w) v = max(v, s_pos[w]);
-    p.acc_len[i] = node_depth(p, node);
+    p.acc_len[i] = s_dep[node];
     p.next_tok[i] = v;
     if (p.acc_node) p.acc_node[i] = node;
   }
@@ -786,7 +826,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_validate(AccParams p, uint32_
         bad |= 1u;
         continue;
       }
-      const float qx = ld(Q, (int64_t)(rq.d0 + node_qrank(p, node_parent(p, n), rq.nq)) * p.p_st + x);
+      const float qx = ld(Q, (int64_t)(rq.d0 + node_rec(p, p.nodes_src, rq, n).pq) * p.p_st + x);
       if (!(qx > 0.f)) bad |= 4u;
     }
   }
@@ -804,7 +844,7 @@ hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_
 hipError_t launch_rowstats(const AccParams& p, hipStream_t s) {
   dim3 block(kAccThreads);
   // independent tree rule: the rows of nodes with children (at least B work-groups)
-  const int64_t rows = p.tree == 1 ? (int64_t)p.B * p.topo.n_inner : (int64_t)p.Nq;
+  const int64_t rows = (p.tree == 1 && !p.per_req) ? (int64_t)p.B * p.topo.n_inner : (int64_t)p.Nq;
   if (p.bf16) {
     constexpr int SUB = RowGeo<uint16_t>::SUB;
     const dim3 grid((unsigned)std::max<int64_t>(rows * ((p.nch + SUB - 1) / SUB), p.B));

@@ -439,16 +439,18 @@ void attn_split_mfma(AttnParams p) {
     }
   };
 
+  const int row_node = (w * 16 + c16 < R) ? (w * 16 + c16) % n : -1;   // this lane's verify node
   {
-    const int r = w * 16 + c16;
-    const int j = (r < R) ? r % n : -1;
     // A uniform loop over the kernel-argument table: each entry is pinned to a
     // scalar register so the selection cannot become a per-lane vector load.
+    // (Per-request trees read their request's masks after the prologue.)
     uint32_t anc = 0u;
-    for (int jj = 0; jj < min(n, kMaxNodes); ++jj) {
-      uint32_t a = p.anc[jj];
-      asm volatile("" : "+s"(a));
-      anc = (j == jj) ? a : anc;
+    if (!p.per_req) {
+      for (int jj = 0; jj < min(n, kMaxNodes); ++jj) {
+        uint32_t a = p.anc[jj];
+        asm volatile("" : "+s"(a));
+        anc = (row_node == jj) ? a : anc;
+      }
     }
     S.anc = anc;
     S.m = -INFINITY;
@@ -477,6 +479,20 @@ void attn_split_mfma(AttnParams p) {
   wait_vm<PER * (NS - 1)>();
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(S.q[ks]));
+  if (p.per_req) {
+    // Per-request trees: this request's ancestor masks from its node-table
+    // entries, by scalar loads (constant address space, wave-uniform
+    // indices) issued while the ring's first tiles are in flight; the first
+    // tile's barrier waits for them.
+    typedef __attribute__((address_space(4))) const uint32_t cu32_t;
+    const cu32_t* na = (const cu32_t*)(p.nodes + it.node0);
+    uint32_t anc = 0u;
+    for (int jj = 0; jj < min(n, kMaxNodes); ++jj) {
+      const uint32_t a = na[2 * jj];             // NodeInfo::anc, the first of its two words
+      anc = (row_node == jj) ? a : anc;
+    }
+    S.anc = anc;
+  }
 
   for (int tb = 0; tb < ntiles; tb += NS) {
     bool stop = false;
@@ -604,7 +620,8 @@ __global__ __launch_bounds__(256) void attn_split_valu(AttnParams p) {
       for (int e = 0; e < D; ++e) s += qs[r][e] * ks[lane][e];
       const int j = r % n;
       s *= p.scale_log2;
-      if (t >= it.ke || !visible(t, ctx, p.anc[j])) s = -INFINITY;
+      const uint32_t anc = p.per_req ? p.nodes[it.node0 + j].anc : p.anc[j];
+      if (t >= it.ke || !visible(t, ctx, anc)) s = -INFINITY;
       const float m_old = ml_s[r][0];
       const float m_new = fmaxf(m_old, wave_max(s));
       const float m_use = (m_new == -INFINITY) ? 0.f : m_new;

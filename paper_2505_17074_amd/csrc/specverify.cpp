@@ -27,6 +27,8 @@ struct Plan {
   // request view
   int B = 0;
   bool tree = false;
+  bool per_req = false;             // a token tree per request
+  std::vector<sv::NodeInfo> nodes;  // per-request trees: every request's node table
   int64_t Nq = 0, Nkv = 0, Nd = 0;
   std::vector<ReqInfo> reqs;
   std::vector<int32_t> row_req;
@@ -41,26 +43,40 @@ struct Plan {
   bool has_acc = false;
   int nch = 0;
   // layout (bytes)
-  size_t off_reqs = 0, off_rowreq = 0, off_items = 0, plan_bytes = 0;
-  size_t off_acc_reqs = 0, off_tickets = 0;
+  size_t off_reqs = 0, off_rowreq = 0, off_items = 0, off_nodes = 0, plan_bytes = 0;
+  size_t off_acc_reqs = 0, off_acc_nodes = 0, off_tickets = 0;
   size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_masses = 0, off_flag = 0;
   size_t device_bytes = 0;
 };
 
+// A BFS parent array: parent[0] = -1, 0 <= parent[n] < n.
+bool valid_tree(const int32_t* parent, int nodes) {
+  if (nodes < 1 || nodes > SPEC_MAX_TREE_NODES || !parent || parent[0] != -1) return false;
+  for (int n = 1; n < nodes; ++n)
+    if (parent[n] < 0 || parent[n] >= n) return false;
+  return true;
+}
+
 spec_status_t check_requests(const spec_requests_t* r) {
   if (!r || r->num_requests < 1 || !r->ctx_len) return SPEC_ERR_INVALID_ARG;
   if (r->tree_nodes < 0 || r->tree_nodes > SPEC_MAX_TREE_NODES) return SPEC_ERR_INVALID_ARG;
-  if (r->tree_nodes > 0) {
-    if (!r->tree_parent || r->tree_parent[0] != -1) return SPEC_ERR_INVALID_ARG;
-    for (int n = 1; n < r->tree_nodes; ++n)
-      if (r->tree_parent[n] < 0 || r->tree_parent[n] >= n) return SPEC_ERR_INVALID_ARG;
+  if (r->node_count) {
+    // per-request trees: no shared tree besides them
+    if (r->tree_nodes != 0 || !r->tree_parents) return SPEC_ERR_INVALID_ARG;
+    int64_t o = 0;
+    for (int i = 0; i < r->num_requests; ++i) {
+      if (!valid_tree(r->tree_parents + o, r->node_count[i])) return SPEC_ERR_INVALID_ARG;
+      o += r->node_count[i];
+    }
+  } else if (r->tree_nodes > 0) {
+    if (!valid_tree(r->tree_parent, r->tree_nodes)) return SPEC_ERR_INVALID_ARG;
   } else if (!r->draft_len) {
     return SPEC_ERR_INVALID_ARG;
   }
   int64_t nq = 0, nkv = 0;
   for (int i = 0; i < r->num_requests; ++i) {
     if (r->ctx_len[i] < 0) return SPEC_ERR_INVALID_ARG;
-    int n = r->tree_nodes;
+    int n = r->node_count ? r->node_count[i] : r->tree_nodes;
     if (n == 0) {
       if (r->draft_len[i] < 0 || r->draft_len[i] > SPEC_MAX_DRAFT) return SPEC_ERR_INVALID_ARG;
       n = r->draft_len[i] + 1;
@@ -213,7 +229,8 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   spec_status_t st = check_requests(r);
   if (st != SPEC_OK) return st;
   P.B = r->num_requests;
-  P.tree = r->tree_nodes > 0;
+  P.per_req = r->node_count != nullptr;
+  P.tree = r->tree_nodes > 0 || P.per_req;
   if (attn) {
     st = check_attn(attn);
     if (st != SPEC_OK) return st;
@@ -229,7 +246,7 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
     P.topo.depth[n] = n;
     P.topo.anc[n] = (n >= 31) ? 0xffffffffu : ((2u << n) - 1u);   // chain: nodes 0..n
   }
-  if (P.tree) {
+  if (P.tree && !P.per_req) {
     std::vector<bool> has_child(tn, false);
     for (int n = 1; n < tn; ++n) has_child[r->tree_parent[n]] = true;
     for (int n = 0; n < tn; ++n) {
@@ -243,21 +260,41 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
     P.topo.n_inner = n_int;
   }
 
-  // requests
+  // requests (and, per-request trees, every request's node table)
   P.reqs.resize(P.B);
-  int64_t q0 = 0, kv0 = 0, d0 = 0;
+  int64_t q0 = 0, kv0 = 0, d0 = 0, o = 0;
   for (int i = 0; i < P.B; ++i) {
     ReqInfo& q = P.reqs[i];
     q.ctx = r->ctx_len[i];
-    q.nq = P.tree ? tn : r->draft_len[i] + 1;
+    q.nq = P.per_req ? r->node_count[i] : (P.tree ? tn : r->draft_len[i] + 1);
     q.q0 = (int32_t)q0;
     q.kv0 = (int32_t)kv0;
     q.d0 = (int32_t)d0;
     q.nseg = 1;
     q.part0 = 0;
+    q.node0 = (int32_t)o;
+    int inner_i = P.tree ? n_int : q.nq - 1;
+    if (P.per_req) {
+      const int32_t* par = r->tree_parents + o;
+      const int nn = q.nq;
+      bool has_child[sv::kMaxNodes] = {};
+      for (int n = 1; n < nn; ++n) has_child[par[n]] = true;
+      inner_i = 0;
+      const size_t base = P.nodes.size();
+      P.nodes.resize(base + nn);
+      for (int n = 0; n < nn; ++n) {
+        sv::NodeInfo& e = P.nodes[base + n];
+        e.parent = (int8_t)par[n];
+        e.depth = (int8_t)(n == 0 ? 0 : P.nodes[base + par[n]].depth + 1);
+        e.anc = (1u << n) | (n == 0 ? 0u : P.nodes[base + par[n]].anc);
+        e.qrank = (int8_t)(has_child[n] ? inner_i++ : -1);
+        e.pqrank = (int8_t)(n == 0 ? -1 : P.nodes[base + par[n]].qrank);
+      }
+      o += nn;
+    }
     q0 += q.nq;
     kv0 += (int64_t)q.ctx + q.nq;
-    d0 += P.tree ? n_int : q.nq - 1;
+    d0 += inner_i;
   }
   P.Nq = q0;
   P.Nkv = kv0;
@@ -335,7 +372,8 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
             it.q0 = q.q0;
             it.kv0 = q.kv0;
             it.part0 = q.part0;
-            it.pad[0] = it.pad[1] = it.pad[2] = it.pad[3] = 0;
+            it.node0 = q.node0;
+            it.pad[0] = it.pad[1] = it.pad[2] = 0;
             P.items.push_back(it);
             nr = std::max(nr, (it.nheads * q.nq + 15) / 16);
           }
@@ -373,9 +411,13 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   off = align_up(off + sizeof(int32_t) * P.Nq);
   P.off_items = off;
   off = align_up(off + sizeof(AttnItem) * P.items.size());
+  P.off_nodes = off;                   // per-request trees: the node table
+  off = align_up(off + sizeof(sv::NodeInfo) * P.nodes.size());
   P.plan_bytes = off;
   P.off_acc_reqs = off;                // the acceptance kernels' copy of the table
   off = align_up(off + sizeof(ReqInfo) * (size_t)(P.has_acc ? P.B : 0));
+  P.off_acc_nodes = off;               // and of the node table
+  off = align_up(off + sizeof(sv::NodeInfo) * (P.has_acc ? P.nodes.size() : 0));
   P.off_tickets = off;                 // acceptance tickets, cleared on the device
   off = align_up(off + sizeof(int32_t) * (size_t)(P.has_acc ? P.B : 0));
   const int D = attn ? attn->head_dim : 0;
@@ -434,6 +476,7 @@ void write_staging(const Plan& P, void* host) {
   std::memcpy(h + P.off_reqs, P.reqs.data(), sizeof(ReqInfo) * P.reqs.size());
   if (!P.items.empty()) std::memcpy(h + P.off_items, P.items.data(), sizeof(AttnItem) * P.items.size());
   std::memcpy(h + P.off_rowreq, P.row_req.data(), sizeof(int32_t) * P.row_req.size());
+  if (!P.nodes.empty()) std::memcpy(h + P.off_nodes, P.nodes.data(), sizeof(sv::NodeInfo) * P.nodes.size());
 }
 
 // How run() places the work: the normal entry points overlap the two parts
@@ -514,6 +557,8 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     a.num_pages = attn->num_pages;
     a.page_bytes = (int64_t)attn->page_tokens * attn->kv_stride_tok * 2;
     std::memcpy(a.anc, P.topo.anc, sizeof(a.anc));
+    a.nodes = reinterpret_cast<const sv::NodeInfo*>(pl + P.off_nodes);
+    a.per_req = P.per_req ? 1 : 0;
   }
   sv::AccParams c{};
   if (acc) {
@@ -538,6 +583,10 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     c.Nq = (int32_t)P.Nq;
     c.tree = P.tree ? (acc->tree_rule == SPEC_TREE_SEQUENTIAL ? 2 : 1) : 0;   // 2: sequential siblings
     c.bf16 = acc->dtype == SPEC_BF16;
+    c.nodes_src = reinterpret_cast<const sv::NodeInfo*>(pl + P.off_nodes);
+    c.nodes = reinterpret_cast<sv::NodeInfo*>(d + P.off_acc_nodes);
+    c.per_req = P.per_req ? 1 : 0;
+    c.nodes_n16 = (int32_t)((sizeof(sv::NodeInfo) * P.nodes.size() + 15) / 16);
   }
 
   // Optional device check of the acceptance inputs (the caller's contract),

@@ -21,8 +21,19 @@ struct ReqInfo {
   int32_t d0;       // first draft-probability row
   int32_t nseg;     // KV splits of this request (1 = direct output)
   int32_t part0;    // first partial row (nseg > 1)
-  int32_t pad;
+  int32_t node0;    // first entry of the request's node table (per-request trees)
 };
+
+// One node of a per-request token tree (the staged node table, and the
+// acceptance kernels' device copy of it).
+struct NodeInfo {
+  uint32_t anc;     // ancestors-or-self bit mask
+  int8_t parent;    // -1 for the root
+  int8_t qrank;     // the request's draft-probability row of this node (nodes with children), else -1
+  int8_t depth;
+  int8_t pqrank;    // qrank of the parent (-1 for the root)
+};
+static_assert(sizeof(NodeInfo) == 8, "8-byte node entries");
 
 // One attention work item: a KV range of one (request, KV head, query-head group).
 // The request's fields are repeated here so a work-group needs one scalar
@@ -39,7 +50,8 @@ struct AttnItem {
   int32_t q0;
   int32_t kv0;
   int32_t part0;
-  int32_t pad[4];
+  int32_t node0;    // the request's first node-table entry (per-request trees)
+  int32_t pad[3];
 };
 
 static_assert(sizeof(ReqInfo) == 32, "ReqInfo is copied as two 16-byte units");
@@ -91,6 +103,10 @@ struct AttnParams {
   int32_t num_pages;
   int64_t page_bytes;
   uint32_t anc[kMaxNodes];   // ancestors-or-self masks (kernel arguments: uniform loads)
+  // per-request trees (per_req = 1): each request's masks in its node-table
+  // entries, read where the host staged them
+  const NodeInfo* nodes;
+  int32_t per_req;
 };
 
 // Acceptance scratch: per (row, vocabulary chunk) max and fp64 sum of exp.
@@ -129,6 +145,12 @@ struct AccParams {
   int32_t tree;        // 1 = tree mode
   int32_t bf16;
   Topo topo;           // kernel arguments: node tables without a memory round trip
+  // per-request trees (per_req = 1): the node table where the host staged it,
+  // and the device copy the row-statistics kernel makes (nodes_n16 16-byte units)
+  const NodeInfo* nodes_src;
+  NodeInfo* nodes;
+  int32_t per_req;
+  int32_t nodes_n16;
 };
 
 constexpr int kAccMaxChunks = 1024;    // vocabularies up to 4M entries

@@ -146,13 +146,24 @@ class Pool:
     draft_probs: np.ndarray      # [Nd, V]
     draft_tokens: np.ndarray     # int32 [Nq - B]
     uniforms: np.ndarray         # float32 [Nq]
+    tree_parents: Optional[list] = None   # per request, its own BFS parent array (instead of tree_parent)
 
     @property
     def batch(self) -> int:
         return int(self.ctx_len.shape[0])
 
     @property
+    def is_tree(self) -> bool:
+        return self.tree_parent is not None or self.tree_parents is not None
+
+    def parents_of(self, i: int):
+        """Request i's tree (BFS parent array), or None for a chain."""
+        return self.tree_parents[i] if self.tree_parents is not None else self.tree_parent
+
+    @property
     def n_q(self) -> np.ndarray:
+        if self.tree_parents is not None:
+            return np.array([len(p) for p in self.tree_parents], dtype=np.int64)
         if self.tree_parent is not None:
             return np.full(self.batch, len(self.tree_parent), dtype=np.int64)
         return self.draft_len.astype(np.int64) + 1
@@ -160,6 +171,8 @@ class Pool:
     @property
     def n_internal(self) -> np.ndarray:
         """Draft-probability rows per request (nodes that have children)."""
+        if self.tree_parents is not None:
+            return np.array([len(set(int(x) for x in p[1:])) for p in self.tree_parents], dtype=np.int64)
         if self.tree_parent is not None:
             ni = len(set(int(p) for p in self.tree_parent[1:]))
             return np.full(self.batch, ni, dtype=np.int64)
@@ -347,16 +360,17 @@ def workload_bytes(pool: Pool) -> dict:
     Nkv = int((pool.ctx_len.astype(np.int64) + n_q).sum())
     d, Hq, Hkv, V, B = pool.head_dim, pool.num_q_heads, pool.num_kv_heads, pool.vocab, pool.batch
     attn_bytes = Nkv * Hkv * d * 2 * s_kv + Nq * Hq * d * s_kv + Nq * Hq * d * 4
-    if pool.tree_parent is not None:
-        par = pool.tree_parent
-        depth = np.zeros(len(par), np.int64)
-        for n in range(1, len(par)):
-            depth[n] = depth[par[n]] + 1
-        vis = int(sum(depth[j] + 1 for j in range(len(par))))
-        flops = 4 * d * Hq * int(sum(int(c) * len(par) + vis for c in pool.ctx_len))
-    else:
-        flops = 4 * d * Hq * int(sum(int(c) * int(n) + int(n) * (int(n) + 1) // 2
-                                     for c, n in zip(pool.ctx_len, n_q)))
+    flops = 0
+    for i in range(B):
+        c, n, par = int(pool.ctx_len[i]), int(n_q[i]), pool.parents_of(i)
+        if par is None:
+            vis = n * (n + 1) // 2
+        else:
+            depth = np.zeros(len(par), np.int64)
+            for m in range(1, len(par)):
+                depth[m] = depth[par[m]] + 1
+            vis = int(sum(depth[j] + 1 for j in range(len(par))))
+        flops += 4 * d * Hq * (c * n + vis)
     acc_bytes = Nq * V * s_l + B * V * s_l + (Nq - B) * (4 + s_l) + Nq * 4 + 8 * B
     return {"attn_bytes": int(attn_bytes), "attn_flops": int(flops), "accept_bytes": int(acc_bytes),
             "Nq": Nq, "Nkv": Nkv}
@@ -373,7 +387,15 @@ def accept_bytes_read(pool: Pool, accepted_node: np.ndarray) -> int:
     n_q = pool.n_q
     Nq, V, B = int(n_q.sum()), pool.vocab, pool.batch
     node = np.asarray(accepted_node, np.int64)
-    if pool.tree_parent is not None:
+    if pool.tree_parents is not None:
+        # per-request trees: every row's statistics are taken
+        rows, qrows = Nq, 0
+        for i in range(B):
+            par = np.asarray(pool.tree_parents[i])
+            inner = np.zeros(len(par), bool)
+            inner[par[1:]] = True
+            qrows += int(inner[node[i]])
+    elif pool.tree_parent is not None:
         par = pool.tree_parent
         inner = np.zeros(len(par), bool)
         inner[par[1:]] = True

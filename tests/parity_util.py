@@ -52,7 +52,7 @@ def oracle_attention_rows(pool: W.Pool, reqs) -> dict:
         n, c = int(n_q[i]), int(pool.ctx_len[i])
         res[i] = verify_attention(pool.q[q0[i]:q0[i] + n], pool.k[kv0[i]:kv0[i + 1]], pool.v[kv0[i]:kv0[i + 1]],
                                   [c], [n], pool.num_kv_heads, dtype=pool.qkv_dtype,
-                                  tree_parent=pool.tree_parent)
+                                  tree_parent=pool.parents_of(i))
     return res
 
 
@@ -66,9 +66,10 @@ def attention_ratios(gpu_out: np.ndarray, pool: W.Pool, ref: dict) -> np.ndarray
     return np.concatenate(out)
 
 
-def oracle_accept(pool: W.Pool, reqs=None) -> dict:
+def oracle_accept(pool: W.Pool, reqs=None, tree_rule: str = "independent") -> dict:
     return verify_accept(pool.target_logits, pool.draft_probs, pool.draft_tokens, pool.uniforms,
-                         pool.n_q, dtype=pool.logit_dtype, tree_parent=pool.tree_parent, requests=reqs)
+                         pool.n_q, dtype=pool.logit_dtype, tree_parent=pool.tree_parent, requests=reqs,
+                         tree_parents=pool.tree_parents, tree_rule=tree_rule)
 
 
 def compare_accept(gpu: dict, ref: dict, pool: W.Pool, reqs=None):
@@ -76,7 +77,7 @@ def compare_accept(gpu: dict, ref: dict, pool: W.Pool, reqs=None):
     Callers assert that the first is empty and the second at most
     max_near_ties(batch)."""
     reqs = range(pool.batch) if reqs is None else reqs
-    max_len = pool.draft_len if pool.tree_parent is None else np.full(pool.batch, int(pool.draft_len.max()))
+    max_len = pool.draft_len
     bad, ties = [], 0
     for i in reqs:
         a, t = int(gpu["accepted_len"][i]), int(gpu["next_token"][i])
@@ -92,22 +93,25 @@ def compare_accept(gpu: dict, ref: dict, pool: W.Pool, reqs=None):
 
 
 def custom_pool(ctx, k=None, tree_parent=None, Hq=8, Hkv=2, d=128, V=1000, qkv=W.BF16, logit=W.F32,
-                seed=0, sigma=1.0) -> W.Pool:
-    """A pool with explicit per-request shapes, drawn with the standard recipe."""
+                seed=0, sigma=1.0, tree_parents=None) -> W.Pool:
+    """A pool with explicit per-request shapes, drawn with the standard recipe.
+    Chains (k per request), one shared tree (tree_parent) or a tree per
+    request (tree_parents)."""
     cfg = W.Config("custom", 99, len(ctx), ("const", 0), ("const", 0), Hq, Hkv, d, qkv, logit, V,
                    ("const", sigma))
     rng = np.random.default_rng(seed)
     ctx = np.asarray(ctx, np.int32)
     B = len(ctx)
-    if tree_parent is not None:
-        par = np.asarray(tree_parent, np.int32)
-        n_q = np.full(B, len(par), np.int64)
-        klen = np.full(B, 0, np.int32)
-        internal = sorted(set(int(x) for x in par[1:]))
+    if tree_parents is not None:
+        pars = [np.asarray(x, np.int32) for x in tree_parents]
+    elif tree_parent is not None:
+        pars = [np.asarray(tree_parent, np.int32)] * B
     else:
-        par = None
-        klen = np.asarray(k, np.int32)
-        n_q = klen.astype(np.int64) + 1
+        pars = [None] * B
+    if tree_parents is not None or tree_parent is not None:
+        n_q = np.array([len(x) for x in pars], np.int64)
+    else:
+        n_q = np.asarray(k, np.int64) + 1
     Nq, Nkv = int(n_q.sum()), int((ctx + n_q).sum())
     q = W.storage(rng.standard_normal((Nq, Hq, d), dtype=np.float32), qkv)
     kk = W.storage(rng.standard_normal((Nkv, Hkv, d), dtype=np.float32), qkv)
@@ -118,11 +122,11 @@ def custom_pool(ctx, k=None, tree_parent=None, Hq=8, Hkv=2, d=128, V=1000, qkv=W
     rows, srcs, toks = [], [], []
     for i in range(B):
         n = int(n_q[i])
-        loc = list(range(n - 1)) if par is None else internal
+        loc = list(range(n - 1)) if pars[i] is None else sorted(set(int(x) for x in pars[i][1:]))
         base = len(rows)
         rows.extend(int(q_start[i]) + x for x in loc)
         for node in range(1, n):
-            parent = node - 1 if par is None else int(par[node])
+            parent = node - 1 if pars[i] is None else int(pars[i][node])
             srcs.append(base + loc.index(parent))
     probs64 = np.exp(dl[rows] - dl[rows].max(-1, keepdims=True)) if rows else np.zeros((0, V))
     if rows:
@@ -133,13 +137,18 @@ def custom_pool(ctx, k=None, tree_parent=None, Hq=8, Hkv=2, d=128, V=1000, qkv=W
         cdf = np.cumsum(stored[s]) / stored[s].sum()
         toks.append(min(int(np.searchsorted(cdf, rng.random(), side="right")), V - 1))
     uni = (rng.integers(0, 1 << 24, size=Nq) * 2.0 ** -24).astype(np.float32)
-    if par is not None:
-        depth = np.zeros(len(par), np.int64)
-        for node in range(1, len(par)):
-            depth[node] = depth[par[node]] + 1
-        klen = np.full(B, int(depth.max()), np.int32)
-    return W.Pool(dataclasses.replace(cfg, batch=B), seed, ctx, klen, par, np.full(B, sigma), Hq, Hkv, d, qkv,
-                  logit, V, q, kk, vv, tl, probs, np.asarray(toks, np.int32), uni)
+    klen = n_q.astype(np.int32) - 1
+    if tree_parents is not None or tree_parent is not None:
+        klen = np.zeros(B, np.int32)
+        for i in range(B):
+            depth = np.zeros(len(pars[i]), np.int64)
+            for node in range(1, len(pars[i])):
+                depth[node] = depth[pars[i][node]] + 1
+            klen[i] = int(depth.max())
+    shared = np.asarray(tree_parent, np.int32) if tree_parent is not None else None
+    return W.Pool(dataclasses.replace(cfg, batch=B), seed, ctx, klen, shared, np.full(B, sigma), Hq, Hkv, d, qkv,
+                  logit, V, q, kk, vv, tl, probs, np.asarray(toks, np.int32), uni,
+                  tree_parents=None if tree_parents is None else [list(map(int, x)) for x in pars])
 
 
 def hand_packed_case():
@@ -176,4 +185,46 @@ def hand_packed_case():
                   uniforms=np.array([0.25, 0.75, 0.625, 0.5, 0.2], np.float32),
                   ctx=np.array([5, 9], np.int32), draft_len=np.array([2, 1], np.int32))
     expect = dict(accepted_len=[1, 0], next_token=[3, 2])
+    return inputs, expect
+
+
+def hand_packed_trees():
+    """Two requests with their own token trees, packed by hand, outputs
+    worked by hand under both tree rules (the SpecInfer token-tree setup of
+    Sec. 5.1; acceptance by Eq. (1), residuals as in Sec. 2.2).
+
+    Vocabulary 4.  Request 0: a root with two children (parents -1, 0, 0):
+    target rows 0-2, one draft row (the root's, row 0), node tokens at 0-1,
+    uniforms at 0-2.  Request 1: a root with one child (parents -1, 0):
+    target rows 3-4, draft row 1, its token at q0 - i = 3 - 1 = 2, uniforms
+    at 3-4.
+
+    Independent rule, request 0: node 1 (token 1) against the root's rows,
+    p(1) = 1/4, q(1) = 1/2, u = 3/4: u q = 3/8 >= 1/4, rejected; node 2
+    (token 2), p(2) = 1/8, q(2) = 1/8, u = 1/4: 1/32 < 1/8, accepted.  The
+    deepest accepted node is node 2, a leaf: the final token comes from its
+    target row (1/8, 1/8, 1/4, 1/2) with u = 5/8, cumulative (1/8, 1/4, 1/2,
+    1): token 3.
+    Sequential rule, request 0: node 1 rejected as above; the running
+    distribution becomes max(0, p - q) = (1/4, 0, 0, 0) normalised =
+    (1, 0, 0, 0); node 2 then has p'(2) = 0: rejected; p' stays (1, 0, 0, 0)
+    after the second update; no child left, so the final token is drawn
+    from p' at the root: token 0, accepted length 0.
+    Request 1 under both rules: node 1 (token 3), p(3) = 1/2, q(3) = 1/4,
+    u = 1/2: 1/8 < 1/2, accepted; node 1 is a leaf: its target row (1/8,
+    3/8, 1/4, 1/4) with u = 3/10, cumulative (1/8, 1/2, 3/4, 1): token 1.
+    """
+    p = np.array([[1 / 2, 1 / 4, 1 / 8, 1 / 8],      # request 0, root
+                  [1 / 4, 1 / 4, 1 / 4, 1 / 4],      # request 0, node 1
+                  [1 / 8, 1 / 8, 1 / 4, 1 / 2],      # request 0, node 2
+                  [1 / 16, 1 / 16, 3 / 8, 1 / 2],    # request 1, root
+                  [1 / 8, 3 / 8, 1 / 4, 1 / 4]])     # request 1, node 1
+    q = np.array([[1 / 4, 1 / 2, 1 / 8, 1 / 8],      # request 0, the root's draft row
+                  [1 / 4, 1 / 4, 1 / 4, 1 / 4]], np.float32)   # request 1, the root's draft row
+    inputs = dict(target_logits=np.log(p).astype(np.float32), draft_probs=q,
+                  draft_tokens=np.array([1, 2, 3], np.int32),
+                  uniforms=np.array([0.75, 0.25, 0.625, 0.5, 0.3], np.float32),
+                  ctx=np.array([4, 7], np.int32), parents=[[-1, 0, 0], [-1, 0]])
+    expect = {"independent": dict(accepted_len=[1, 1], next_token=[3, 1], accepted_node=[2, 1]),
+              "sequential": dict(accepted_len=[0, 1], next_token=[0, 1], accepted_node=[0, 1])}
     return inputs, expect

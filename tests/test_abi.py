@@ -281,3 +281,45 @@ def test_noalloc_checks_before_any_hip_call(lib):
     text = open(HEADER).read()
     assert "#define SPEC_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)" in text
     assert "#define SPEC_NOALLOC_STAGING_BYTES ((size_t)1 << 20)" in text
+
+
+def _req_trees(ctx, parents):
+    return B.make_requests(np.array(ctx), None, None, tree_parents=parents)
+
+
+@pytest.mark.parametrize("parents,expect", [
+    ([[-1, 0, 0], [-1]], B.SPEC_OK),
+    ([[-1, 0, 0], [-1, 0, 1, 1]], B.SPEC_OK),
+    ([[-1, 0, 0], [0, 0]], B.SPEC_ERR_INVALID_ARG),          # root's parent must be -1
+    ([[-1, 0, 2], [-1]], B.SPEC_ERR_INVALID_ARG),            # parent[n] < n
+    ([[-1, 0, 0], [-1] + list(range(32))], B.SPEC_ERR_INVALID_ARG),   # 33 nodes
+    ([[-1] + list(range(31)), [-1]], B.SPEC_OK),             # 32 nodes
+])
+def test_per_request_tree_checks(lib, parents, expect):
+    assert _ws(_req_trees([5, 9], parents), _attn(), _acc())[0] == expect
+
+
+def test_per_request_trees_exclude_a_shared_tree_and_empty_trees(lib):
+    r = _req_trees([5, 9], [[-1, 0], [-1]])
+    par = np.array([-1, 0], np.int32)
+    r.tree_nodes, r.tree_parent = 2, par.ctypes.data_as(C.POINTER(C.c_int32))
+    assert _ws(r, _attn(), _acc())[0] == B.SPEC_ERR_INVALID_ARG
+    r = _req_trees([5, 9], [[-1, 0], [-1]])
+    cnt = np.array([2, 0], np.int32)                           # a request with no node
+    r.node_count = cnt.ctypes.data_as(C.POINTER(C.c_int32))
+    assert _ws(r, _attn(), _acc())[0] == B.SPEC_ERR_INVALID_ARG
+    r = _req_trees([5, 9], [[-1, 0], [-1]])
+    r.tree_parents = C.POINTER(C.c_int32)()
+    assert _ws(r, _attn(), _acc())[0] == B.SPEC_ERR_INVALID_ARG
+
+
+def test_per_request_trees_size_like_the_shared_tree(lib):
+    """Per-request trees that are all one shared tree need the shared tree's
+    device workspace plus the acceptance kernels' copy of the node table, and
+    the staged node table (8 bytes per node) on top of the shared plan."""
+    tree = [-1, 0, 0, 1, 1, 2, 2]
+    ctx = [5, 9, 300]
+    shared = _ws(B.make_requests(np.array(ctx), None, tree), _attn(), _acc())
+    per = _ws(_req_trees(ctx, [tree] * 3), _attn(), _acc())
+    assert shared[0] == per[0] == B.SPEC_OK
+    assert per[2] >= shared[2] + 8 * 21 and per[1] >= shared[1] + 8 * 21

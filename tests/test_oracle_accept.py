@@ -218,6 +218,48 @@ def test_batch_packing_by_hand():
     assert not r["near_tie"].any()
 
 
+@pytest.mark.parametrize("rule", ["independent", "sequential"])
+def test_per_request_trees_by_hand(rule):
+    """Per-request topologies: the packing (target rows and uniforms at q0_i,
+    node tokens at q0_i - i, draft rows at d0_i = running count of nodes with
+    children) against a two-request case worked by hand under each rule."""
+    from parity_util import hand_packed_trees
+    inp, expect = hand_packed_trees()
+    r = verify_accept(inp["target_logits"], inp["draft_probs"], inp["draft_tokens"], inp["uniforms"],
+                      [len(x) for x in inp["parents"]], tree_parents=inp["parents"], tree_rule=rule)
+    for key, val in expect[rule].items():
+        assert r[key].tolist() == val, (rule, key, r[key])
+    assert not r["near_tie"].any()
+
+
+@pytest.mark.parametrize("rule", ["independent", "sequential"])
+def test_per_request_paths_and_shared_trees(rule):
+    """Per-request trees that are all paths decide exactly as chains; per-request
+    trees that are all equal decide exactly as the shared tree."""
+    rng = np.random.default_rng(8)
+    V = 32
+    n_q = [4, 1, 6, 3]
+    logits = rng.standard_normal((sum(n_q), V)).astype(np.float32)
+    probs = np.stack([_dist(V, rng) for _ in range(sum(n_q) - len(n_q))]).astype(np.float32)
+    toks = rng.integers(0, V, size=sum(n_q) - len(n_q)).astype(np.int32)
+    us = rng.random(sum(n_q)).astype(np.float32)
+    chain = verify_accept(logits, probs, toks, us, n_q)
+    paths = verify_accept(logits, probs, toks, us, n_q, tree_parents=[list(range(-1, n - 1)) for n in n_q],
+                          tree_rule=rule)
+    for key in ("accepted_len", "next_token", "accepted_node", "near_tie"):
+        np.testing.assert_array_equal(chain[key], paths[key])
+    tree = [-1, 0, 0, 1, 1, 2]
+    B = 5
+    logits = rng.standard_normal((6 * B, V)).astype(np.float32)
+    probs = np.stack([_dist(V, rng) for _ in range(3 * B)]).astype(np.float32)
+    toks = rng.integers(0, V, size=5 * B).astype(np.int32)
+    us = rng.random(6 * B).astype(np.float32)
+    shared = verify_accept(logits, probs, toks, us, [6] * B, tree_parent=tree, tree_rule=rule)
+    per = verify_accept(logits, probs, toks, us, [6] * B, tree_parents=[tree] * B, tree_rule=rule)
+    for key in ("accepted_len", "next_token", "accepted_node", "near_tie"):
+        np.testing.assert_array_equal(shared[key], per[key])
+
+
 # ------------------------------------------------------------------- trees
 def test_path_tree_equals_chain_batch():
     rng = np.random.default_rng(3)

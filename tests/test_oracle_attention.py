@@ -25,13 +25,16 @@ def _batch(ctx, n_q, Hq, Hkv, d, rng=RNG):
     return _rand((Nq, Hq, d), rng), _rand((Nkv, Hkv, d), rng), _rand((Nkv, Hkv, d), rng)
 
 
-def _sdpa(q, k, v, ctx, n_q, Hkv, parent=None):
-    """Independent reference: torch SDPA in fp64 with repeated KV heads."""
+def _sdpa(q, k, v, ctx, n_q, Hkv, parent=None, parents=None):
+    """Independent reference: torch SDPA in fp64 with repeated KV heads
+    (parents: a parent array per request)."""
     Hq = q.shape[1]
     G = Hq // Hkv
     out = np.zeros(q.shape, np.float64)
     q0 = kv0 = 0
-    for c, n in zip(ctx, n_q):
+    for i, (c, n) in enumerate(zip(ctx, n_q)):
+        if parents is not None:
+            parent = parents[i]
         L = c + n
         mask = torch.zeros(n, L, dtype=torch.bool)
         mask[:, :c] = True
@@ -72,6 +75,33 @@ def test_matches_torch_sdpa_tree():
     ours = verify_attention(q, k, v, ctx, n_q, 2, tree_parent=parent)
     ref = _sdpa(q, k, v, ctx, n_q, 2, parent=parent)
     np.testing.assert_allclose(ours, ref, rtol=1e-12, atol=1e-12)
+
+
+# per-request topologies: a path, a binary tree, a wide root, a lone root,
+# a non-binary tree
+PER_REQUEST = [[-1, 0, 1, 2], [-1, 0, 0, 1, 1, 2, 2], [-1, 0, 0, 0, 0], [-1], [-1, 0, 0, 1, 1, 1, 3]]
+
+
+def test_matches_torch_sdpa_per_request_trees():
+    ctx = [3, 0, 9, 4, 1]
+    n_q = [len(p) for p in PER_REQUEST]
+    q, k, v = _batch(ctx, n_q, 4, 2, 8)
+    ours = verify_attention(q, k, v, ctx, n_q, 2, tree_parents=PER_REQUEST)
+    ref = _sdpa(q, k, v, ctx, n_q, 2, parents=PER_REQUEST)
+    np.testing.assert_allclose(ours, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_per_request_paths_are_chains_and_shared_trees_agree():
+    ctx = [3, 0, 9]
+    n_q = [4, 2, 5]
+    q, k, v = _batch(ctx, n_q, 4, 2, 8)
+    paths = [list(range(-1, n - 1)) for n in n_q]
+    np.testing.assert_array_equal(verify_attention(q, k, v, ctx, n_q, 2, tree_parents=paths),
+                                  verify_attention(q, k, v, ctx, n_q, 2))
+    tree = [-1, 0, 0, 1, 2]
+    q, k, v = _batch(ctx, [5] * 3, 4, 2, 8)
+    np.testing.assert_array_equal(verify_attention(q, k, v, ctx, [5] * 3, 2, tree_parents=[tree] * 3),
+                                  verify_attention(q, k, v, ctx, [5] * 3, 2, tree_parent=tree))
 
 
 def test_single_visible_key_returns_its_value():
