@@ -249,6 +249,33 @@ typedef struct spec_accept_args {
   int32_t pad0;
 } spec_accept_args_t;
 
+/*
+ * The target model's LM head (device memory): the verify positions' logits
+ * logits = hidden . weight^T, the forward that produces the target
+ * distributions the acceptance test of Eq. (1) compares with the draft's
+ * (Sec. 2.2).
+ *   hidden  [Nq, hidden_dim] bf16: the final hidden state of each verify
+ *           position (row r = verify position r), row stride hidden_stride
+ *           elements.
+ *   weight  [vocab, hidden_dim] bf16: the LM head's weight, one row per
+ *           vocabulary entry, row stride weight_stride elements.
+ *   hidden_dim a positive multiple of 32; strides >= hidden_dim and
+ *   multiples of 8; both pointers 16-byte aligned.  The products accumulate
+ *   in fp32 (bf16 x bf16 products are exact in fp32).
+ *   event_begin / event_end: optional hipEvent_t recorded on `stream` right
+ *   before and right after the GEMM kernel (NULL = none).
+ */
+typedef struct spec_lm_head_args {
+  int32_t hidden_dim;
+  int32_t pad0;
+  const void* hidden;
+  int64_t hidden_stride;
+  const void* weight;
+  int64_t weight_stride;
+  void* event_begin;
+  void* event_end;
+} spec_lm_head_args_t;
+
 /* Workspace sizes for a call with these arguments (either args pointer may
  * be NULL when that part is not run).  The device workspace must be
  * 256-byte aligned; the host staging buffer should be pinned
@@ -311,6 +338,30 @@ SPEC_API spec_status_t spec_verify_noalloc(const spec_requests_t* req,
                                            const spec_attn_args_t* attn,
                                            const spec_accept_args_t* acc,
                                            void* stream);
+
+/* The LM head fused with acceptance and the final sample: the GEMM writes
+ * the logits once into acc->target_logits (an OUTPUT here: [Nq, vocab] in
+ * acc->dtype, fp32 or rounded to bf16, row stride acc->logits_stride) and,
+ * in its epilogue, the maximum and the sum of exp(l - max) of every
+ * (row, 256-entry tile) of the stored logits; the acceptance then folds those
+ * into its normalisers instead of streaming the logits again, and reads the
+ * logits only for its tests and the final sample.  Results equal spec_accept
+ * on the same logits except where u * S lies within rounding of a boundary
+ * (both are exact up to fp32 rounding of the normalisers).  Everything runs
+ * on `stream`.  Workspace sizes from spec_lm_head_workspace_bytes. */
+SPEC_API spec_status_t spec_lm_head_accept(const spec_requests_t* req,
+                                           const spec_lm_head_args_t* lm,
+                                           const spec_accept_args_t* acc,
+                                           void* workspace, size_t workspace_bytes,
+                                           void* host_staging, size_t host_staging_bytes,
+                                           void* stream);
+
+/* Workspace sizes for spec_lm_head_accept (as spec_workspace_bytes). */
+SPEC_API spec_status_t spec_lm_head_workspace_bytes(const spec_requests_t* req,
+                                                    const spec_lm_head_args_t* lm,
+                                                    const spec_accept_args_t* acc,
+                                                    size_t* device_bytes,
+                                                    size_t* host_bytes);
 
 /* Static text for a status code. */
 SPEC_API const char* spec_status_str(spec_status_t status);

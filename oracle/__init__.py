@@ -19,6 +19,10 @@ What it computes (each function cites the passage it follows):
   distribution on rejection (Sec. 2.2), and the one extra LLM token when every
   candidate is accepted (Sec. 4.3, the "+1" of Eq. (6)).
 
+* ``lm_head.lm_head_logits`` -- the target model's LM head over the verify
+  positions' final hidden states (the forward of Sec. 2.2 whose output is
+  the target distributions of Eq. (1)).
+
 * ``scheduler.simulate`` -- the LAPS-SD request scheduler of Algorithm 1
   (Sec. 4: priority queues with exponential thresholds, demotion by attained
   service, the acceptance-rate stability test, the Eq. (6) estimate, and
@@ -31,5 +35,6 @@ widen to fp64 exactly).  Both parts are exact results with a plain definition,
 so the oracle is that definition written out, not an approximation.
 """
 from .attention import verify_attention, ancestors_or_self, widen  # noqa: F401
+from .lm_head import lm_head_logits  # noqa: F401
 from .accept import (accept_chain, accept_tree, accept_tree_sequential, verify_accept, softmax64,  # noqa: F401
                      inverse_cdf, NEAR_TIE, NEAR_TIE_MASS)

@@ -235,3 +235,70 @@ class PagedKV:
         a.block_table = self.table.data_ptr()
         a.block_stride, a.page_tokens, a.num_pages = self.block_stride, self.page_tokens, self.num_pages
         return a
+
+
+def pad_vocab_rows(batch: DeviceBatch) -> None:
+    """Give the batch's logits and draft rows a row stride padded to 16 bytes
+    (the ABI's row alignment), whatever the vocabulary size."""
+    for attr in ("logits", "probs"):
+        t = getattr(batch, attr)
+        vec = 16 // t.element_size()
+        V = t.shape[1]
+        Vp = -(-V // vec) * vec
+        if Vp != V and t.numel():
+            pad = torch.zeros((t.shape[0], Vp), dtype=t.dtype, device=batch.device)
+            pad[:, :V] = t
+            setattr(batch, attr, pad[:, :V])
+
+
+class LmHeadVerifier:
+    """spec_lm_head_accept on a pool from workload.make_lm_head_pool: the
+    hidden states and LM-head weights in device memory, the logits buffer
+    the GEMM writes (then read by the acceptance), the draft inputs and the
+    outputs; a device workspace and one pinned staging buffer (each call
+    waits for the previous one before rewriting it)."""
+
+    def __init__(self, pool: Pool, device="cuda"):
+        if pool.hidden is None or pool.weight is None:
+            raise ValueError("the pool carries no LM-head inputs")
+        self.batch = DeviceBatch(pool, device)        # logits buffer (zeros), draft rows, tokens, uniforms, outputs
+        dev = self.batch.device
+        pad_vocab_rows(self.batch)
+        self.hidden = torch.from_numpy(np.ascontiguousarray(pool.hidden).view(np.int16)).view(torch.bfloat16).to(dev)
+        self.weight = torch.from_numpy(np.ascontiguousarray(pool.weight).view(np.int16)).view(torch.bfloat16).to(dev)
+        self.req = self.batch.requests()
+        self.lm = B.SpecLmHeadArgs()
+        self.lm.hidden_dim = int(pool.hidden.shape[1])
+        self.lm.hidden, self.lm.hidden_stride = self.hidden.data_ptr(), self.hidden.stride(0)
+        self.lm.weight, self.lm.weight_stride = self.weight.data_ptr(), self.weight.stride(0)
+        self.acc = self.batch.accept_args()
+        st, dbytes, hbytes = B.spec_lm_head_workspace_bytes(self.req, self.lm, self.acc)
+        B.check(st, "spec_lm_head_workspace_bytes")
+        self.ws_bytes = dbytes
+        self._ws = torch.empty(dbytes + 256, dtype=torch.uint8, device=dev)
+        self.ws_ptr = (self._ws.data_ptr() + 255) // 256 * 256
+        self.staging_bytes = hbytes
+        self._staging = torch.empty(max(hbytes, 1), dtype=torch.uint8, pin_memory=True)
+        self._done = None
+
+    def run(self, stream: Optional[torch.cuda.Stream] = None) -> None:
+        stream = stream or torch.cuda.current_stream(self.batch.device)
+        if self._done is not None:
+            self._done.synchronize()      # the staging buffer is rewritten by this call
+        st = B.spec_lm_head_accept(self.req, self.lm, self.acc, self.ws_ptr, self.ws_bytes,
+                                   self._staging.data_ptr(), self.staging_bytes, stream.cuda_stream)
+        self._done = torch.cuda.Event()
+        self._done.record(stream)
+        B.check(st, "spec_lm_head_accept")
+
+    def logits(self) -> np.ndarray:
+        """The logits the GEMM wrote, in their storage format."""
+        torch.cuda.synchronize(self.batch.device)
+        t = self.batch.logits.contiguous()
+        return t.view(torch.int16).cpu().numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.cpu().numpy()
+
+    def results(self) -> dict:
+        torch.cuda.synchronize(self.batch.device)
+        b = self.batch
+        return {"accepted_len": b.accepted_len.cpu().numpy(), "next_token": b.next_token.cpu().numpy(),
+                "accepted_node": b.accepted_node.cpu().numpy()}

@@ -22,6 +22,7 @@ SPEC_NOALLOC_STAGING_BYTES = 1 << 20
 
 EXPORTS = ("spec_workspace_bytes", "spec_verify_attn", "spec_accept", "spec_verify",
            "spec_status_str", "spec_abi_version", "spec_stream_read_probe", "spec_verify_noalloc",
+           "spec_lm_head_accept", "spec_lm_head_workspace_bytes",
            "spec_sched_create", "spec_sched_destroy", "spec_sched_submit", "spec_sched_next",
            "spec_sched_report", "spec_sched_query", "spec_sched_simulate")
 
@@ -81,6 +82,17 @@ class SpecAcceptArgs(C.Structure):
                 ("event_mid", C.c_void_p),
                 ("tree_rule", C.c_int32),
                 ("pad0", C.c_int32)]
+
+
+class SpecLmHeadArgs(C.Structure):
+    _fields_ = [("hidden_dim", C.c_int32),
+                ("pad0", C.c_int32),
+                ("hidden", C.c_void_p),
+                ("hidden_stride", C.c_int64),
+                ("weight", C.c_void_p),
+                ("weight_stride", C.c_int64),
+                ("event_begin", C.c_void_p),
+                ("event_end", C.c_void_p)]
 
 
 class SpecSchedParams(C.Structure):
@@ -163,6 +175,12 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.spec_verify.restype = C.c_int
     lib.spec_verify_noalloc.argtypes = [P(SpecRequests), P(SpecAttnArgs), P(SpecAcceptArgs), C.c_void_p]
     lib.spec_verify_noalloc.restype = C.c_int
+    lib.spec_lm_head_accept.argtypes = [P(SpecRequests), P(SpecLmHeadArgs), P(SpecAcceptArgs), C.c_void_p,
+                                        C.c_size_t, C.c_void_p, C.c_size_t, C.c_void_p]
+    lib.spec_lm_head_accept.restype = C.c_int
+    lib.spec_lm_head_workspace_bytes.argtypes = [P(SpecRequests), P(SpecLmHeadArgs), P(SpecAcceptArgs),
+                                                 P(C.c_size_t), P(C.c_size_t)]
+    lib.spec_lm_head_workspace_bytes.restype = C.c_int
     lib.spec_status_str.argtypes = [C.c_int]
     lib.spec_status_str.restype = C.c_char_p
     lib.spec_abi_version.argtypes = []
@@ -223,6 +241,17 @@ def spec_verify(req, attn, acc, ws: int, ws_bytes: int, staging: int, staging_by
 
 def spec_verify_noalloc(req, attn, acc, stream: int) -> int:
     return load().spec_verify_noalloc(C.byref(req), _ref(attn), _ref(acc), stream)
+
+
+def spec_lm_head_workspace_bytes(req: SpecRequests, lm: SpecLmHeadArgs, acc: SpecAcceptArgs):
+    """Returns (status, device_bytes, host_bytes)."""
+    dev, host = C.c_size_t(0), C.c_size_t(0)
+    st = load().spec_lm_head_workspace_bytes(C.byref(req), _ref(lm), _ref(acc), C.byref(dev), C.byref(host))
+    return st, dev.value, host.value
+
+
+def spec_lm_head_accept(req, lm, acc, ws: int, ws_bytes: int, staging: int, staging_bytes: int, stream: int) -> int:
+    return load().spec_lm_head_accept(C.byref(req), _ref(lm), _ref(acc), ws, ws_bytes, staging, staging_bytes, stream)
 
 
 def spec_abi_version() -> int:

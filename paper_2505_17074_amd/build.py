@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libspecverify.so")
-SOURCES = ["attention.hip", "accept.hip", "probe.hip", "noalloc.hip", "specverify.cpp", "scheduler.cpp"]
+SOURCES = ["attention.hip", "accept.hip", "probe.hip", "noalloc.hip", "lmhead.hip", "specverify.cpp", "scheduler.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

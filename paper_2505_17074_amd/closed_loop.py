@@ -13,9 +13,13 @@ serves every policy.  The native scheduler (specsched.h) then serves the
 workload under each policy on the server model of Sec. 3.
 
 Times (integer microseconds):
-  * a round lasts n * T_SSM + T_LLM, with T_LLM = 10 ms per verification
-    (the per-token verification time Fig. 1 assumes for LLaMA-7B) and
-    T_SSM = 0.5 ms per drafted token;
+  * a round lasts n * T_SSM + T_LLM + t_verify(c): T_LLM = 10 ms per
+    verification (the per-token verification time Fig. 1 assumes for
+    LLaMA-7B) stands for the target forward outside the verify kernels,
+    T_SSM = 0.5 ms per drafted token, and t_verify(c) is MEASURED on the GPU
+    by `measure_verify`: the verify attention of each of LLaMA-7B's 32
+    decoder layers plus one acceptance, for one request whose context is c
+    (the request's prompt plus half its output);
   * switching swaps a request's KV cache at `swap_us_per_token` per cached
     token each way.  The default of 8 us assumes LLaMA-7B fp16 KV (512 KB
     per token) over a 64 GB/s host link; `measure_swap` times the copies on
@@ -24,7 +28,7 @@ Times (integer microseconds):
 from __future__ import annotations
 
 import dataclasses
-from typing import List
+from typing import List, Optional
 
 import numpy as np
 
@@ -50,6 +54,8 @@ class LoopConfig:
     t_llm_us: int = 10_000
     swap_us_per_token: int = 8
     arrival_frac: float = 0.3          # arrivals uniform over this fraction of the total service
+    layers: int = 32                   # LLaMA-7B decoder layers: one verify attention each per round
+    verify_us: Optional[dict] = None   # measured {context: us} of one round's verify kernels (None: not counted)
 
 
 @dataclasses.dataclass
@@ -92,6 +98,48 @@ def measure_swap(device="cuda", tokens=(16, 64, 256, 1024, 4096), reps: int = 5)
     out["us_per_token"] = int(np.ceil(KV_BYTES_PER_TOKEN / (gbs * 1e9) * 1e6))
     del dev, host
     return out
+
+
+def measure_verify(device="cuda", contexts=(128, 512, 1024, 2048), reps: int = 20, layers: int = 32,
+                   draft: int = 4) -> dict:
+    """One round's verify kernels on this GPU, per context length: the
+    library's verify attention for each of `layers` decoder layers plus one
+    acceptance, for one request of the LLaMA-7B shape (32 heads x 128,
+    `draft` drafts, vocabulary 32000, bf16 KV cache, fp32 logits), timed by
+    events around spec_verify_attn and spec_accept calls.  Returns
+    {context: us}."""
+    import dataclasses as dc
+    import torch
+    from . import workload as W
+    from .batch import DeviceBatch, Verifier
+    base = W.CONFIG_BY_NAME["mha7b_b32"]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = {}
+    for c in contexts:
+        cfg = dc.replace(base, name=f"verify_c{c}", batch=1, ctx=("const", int(c)), draft=("const", draft))
+        b = DeviceBatch(W.make_pool(cfg, 0), device)
+        v = Verifier(b)
+        t = {}
+        for which in ("attn", "accept"):
+            for _ in range(3):
+                v.run(which)
+            e0.record()
+            for _ in range(reps):
+                v.run(which)
+            e1.record()
+            torch.cuda.synchronize()
+            t[which] = e0.elapsed_time(e1) * 1e3 / reps
+        out[int(c)] = layers * t["attn"] + t["accept"]
+        del v, b
+    return out
+
+
+def verify_us_at(cfg: LoopConfig, context: float) -> int:
+    """t_verify at a context length, interpolated in the measured table (0 when none)."""
+    if not cfg.verify_us:
+        return 0
+    xs = sorted(cfg.verify_us)
+    return int(round(float(np.interp(context, xs, [cfg.verify_us[x] for x in xs]))))
 
 
 def make_workload(cfg: LoopConfig, seed: int) -> LoopWorkload:
@@ -164,12 +212,12 @@ def gpu_traces(cfg: LoopConfig, wl: LoopWorkload, seed: int, device="cuda", capt
 
 
 def requests_from(cfg: LoopConfig, wl: LoopWorkload, traces: np.ndarray) -> List[SchedRequest]:
-    round_us = cfg.draft * cfg.t_ssm_us + cfg.t_llm_us
     out = []
     for i in range(cfg.requests):
         L = int(wl.out_len[i])
         acc = np.zeros(max(L, traces.shape[1]), np.int64)
         acc[:traces.shape[1]] = traces[i]
+        round_us = cfg.draft * cfg.t_ssm_us + cfg.t_llm_us + verify_us_at(cfg, int(wl.prompt[i]) + L / 2)
         out.append(SchedRequest(int(wl.arrival[i]), int(wl.prompt[i]), L, int(wl.pred_len[i]), cfg.draft, round_us,
                                 acc))
     return out

@@ -135,16 +135,6 @@ __device__ __forceinline__ void load16_contiguous(const T* row, int base, int V,
   for (int j = 0; j < 16 / VW; ++j) load_vec(row, base + 16 * threadIdx.x + j * VW, V, pad, x + j * VW);
 }
 
-// exp(x - m) for x <= m (a logit against a maximum): the hardware base-2
-// exponential of (x - m) log2 e.  Its error is about an ulp of the result
-// plus the roundings of x - m and of the product, the same order as the
-// library expf, in three instructions instead of a dozen.  Every kernel
-// below evaluates exp(l - m) through this one function, so a statistic and
-// the entries it summarises are always computed alike.
-__device__ __forceinline__ float exp_rel(float x, float m) {
-  return __builtin_amdgcn_exp2f((x - m) * 1.4426950408889634f);
-}
-
 template <typename T>
 struct RowGeo {
   static constexpr int VW = 16 / sizeof(T);                 // entries per 16-byte load
@@ -165,7 +155,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
   // that leaf is chosen, and the decision kernel then takes its statistics.
   // Every request has the tree's `nodes` rows there, so the row is arithmetic.
   int row = su;
-  if (p.tree == 1 && !p.per_req) {
+  if (p.tree == 1 && !p.all_stats) {
     const int ni = p.topo.n_inner;
     row = (ni > 0 && su < p.B * ni) ? (su / ni) * p.topo.nodes + p.topo.inner[su % ni] : -1;
   }
@@ -346,7 +336,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
 
   // (M, Z) of every row of the request that has chunk statistics
   for (int r = wv; r < N; r += kAccThreads / 64) {
-    if (p.tree == 1 && !p.per_req && p.topo.qrank[r] < 0) continue;     // a leaf's row: none yet
+    if (p.tree == 1 && !p.all_stats && p.topo.qrank[r] < 0) continue;     // a leaf's row: none yet
     const ChunkStat* st = p.rowstats + (int64_t)(rq.q0 + r) * p.nch;
     float m = -INFINITY;
     for (int k = ln; k < p.nch; k += 64) m = fmaxf(m, st[k].m);
@@ -396,7 +386,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   const double invZ = 1.0 / d.Z;
   bool residual = d.qrow >= 0;
   // a leaf's row under the independent rule over a shared tree has no statistics yet
-  const bool own_stats = !residual && p.tree == 1 && !p.per_req;
+  const bool own_stats = !residual && p.tree == 1 && !p.all_stats;
   const T* Lr = L + (int64_t)d.row * p.l_st;
   const T* Qr = Q + (int64_t)(d.qrow >= 0 ? d.qrow : 0) * p.p_st;
   ChunkStat* rst = p.rowstats + (int64_t)d.row * p.nch;
@@ -833,7 +823,42 @@ __global__ __launch_bounds__(kAccThreads) void acc_validate(AccParams p, uint32_
   if (bad) atomicOr(flag, bad);
 }
 
+// Chunk statistics from the LM head's tile statistics: thread t of the grid
+// folds the kLmhTilesPerChunk tiles of one (row, chunk) in tile order into
+// (max, sum of exp(l - max)), max over the tiles' maxima and the tiles' sums
+// rescaled in fp64.  The first B work-groups also make the device copies of
+// the request and node tables and clear the tickets, as the row-statistics
+// kernel does on the unfused path.
+__global__ __launch_bounds__(kAccThreads) void acc_foldstats(AccParams p, const ChunkStat* tiles, int ntiles) {
+  if (blockIdx.x < p.B) {
+    if (threadIdx.x < 2)
+      reinterpret_cast<uint4*>(p.reqs + blockIdx.x)[threadIdx.x] =
+          reinterpret_cast<const uint4*>(p.reqs_src + blockIdx.x)[threadIdx.x];
+    if (threadIdx.x == 0) p.tickets[blockIdx.x] = 0;
+    if (p.per_req)
+      for (int x = blockIdx.x * kAccThreads + threadIdx.x; x < p.nodes_n16; x += p.B * kAccThreads)
+        reinterpret_cast<uint4*>(p.nodes)[x] = reinterpret_cast<const uint4*>(p.nodes_src)[x];
+  }
+  const int64_t idx = (int64_t)blockIdx.x * kAccThreads + threadIdx.x;
+  if (idx >= (int64_t)p.Nq * p.nch) return;
+  const int row = (int)(idx / p.nch), c = (int)(idx % p.nch);
+  const int t0 = c * kLmhTilesPerChunk, t1 = min(t0 + kLmhTilesPerChunk, ntiles);
+  const ChunkStat* ts = tiles + (int64_t)row * ntiles;
+  float m = -INFINITY;
+  for (int t = t0; t < t1; ++t) m = fmaxf(m, ts[t].m);
+  double sum = 0.0;
+  for (int t = t0; t < t1; ++t) sum += ts[t].s * exp((double)ts[t].m - (double)m);
+  p.rowstats[idx] = ChunkStat{sum, m, 0.f};
+}
+
 }  // namespace
+
+hipError_t launch_foldstats(const AccParams& p, const ChunkStat* tiles, int ntiles, hipStream_t s) {
+  const int64_t n = (int64_t)p.Nq * p.nch;
+  const dim3 grid((unsigned)std::max<int64_t>((n + kAccThreads - 1) / kAccThreads, p.B));
+  acc_foldstats<<<grid, dim3(kAccThreads), 0, s>>>(p, tiles, ntiles);
+  return hipGetLastError();
+}
 
 hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_t s) {
   if (p.bf16) acc_validate<uint16_t><<<1, kAccThreads, 0, s>>>(p, flag);
@@ -844,7 +869,7 @@ hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_
 hipError_t launch_rowstats(const AccParams& p, hipStream_t s) {
   dim3 block(kAccThreads);
   // independent tree rule: the rows of nodes with children (at least B work-groups)
-  const int64_t rows = (p.tree == 1 && !p.per_req) ? (int64_t)p.B * p.topo.n_inner : (int64_t)p.Nq;
+  const int64_t rows = (p.tree == 1 && !p.all_stats) ? (int64_t)p.B * p.topo.n_inner : (int64_t)p.Nq;
   if (p.bf16) {
     constexpr int SUB = RowGeo<uint16_t>::SUB;
     const dim3 grid((unsigned)std::max<int64_t>(rows * ((p.nch + SUB - 1) / SUB), p.B));

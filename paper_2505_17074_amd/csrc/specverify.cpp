@@ -487,7 +487,36 @@ struct RunMode {
   bool overlap = true;
   bool pageable = false;      // staging known not to be device-mapped
   std::mutex* staging_mu = nullptr;   // held while the staging is written and the copy enqueued
+  const spec_lm_head_args_t* lm = nullptr;   // the LM head runs first, its statistics replace the row pass
+  size_t off_tiles = 0;       // its tile statistics in the workspace
 };
+
+spec_status_t check_lm(const spec_lm_head_args_t* lm) {
+  if (!lm || !lm->hidden || !lm->weight) return SPEC_ERR_INVALID_ARG;
+  if (lm->hidden_dim < 32 || lm->hidden_dim % 32) return SPEC_ERR_INVALID_ARG;
+  if (!aligned16(lm->hidden) || !aligned16(lm->weight)) return SPEC_ERR_INVALID_ARG;
+  if (lm->hidden_stride < lm->hidden_dim || lm->hidden_stride % 8 || lm->weight_stride < lm->hidden_dim ||
+      lm->weight_stride % 8)
+    return SPEC_ERR_INVALID_ARG;
+  // each work-group's rows are addressed with 32-bit offsets
+  if ((int64_t)sv::kLmhNT * lm->weight_stride * 2 >= INT32_MAX || (int64_t)128 * lm->hidden_stride * 2 >= INT32_MAX)
+    return SPEC_ERR_UNSUPPORTED;
+  return SPEC_OK;
+}
+
+// The LM-head call's plan: the acceptance plan plus the tile statistics
+// [Nq, ceil(V / 256)] at the end of the workspace.
+spec_status_t lm_plan(const spec_requests_t* req, const spec_lm_head_args_t* lm, const spec_accept_args_t* acc,
+                      Plan& P, size_t& off_tiles, size_t& device_bytes) {
+  if (!acc) return SPEC_ERR_INVALID_ARG;
+  spec_status_t st = build_plan(req, nullptr, acc, P);
+  if (st != SPEC_OK) return st;
+  if ((st = check_lm(lm)) != SPEC_OK) return st;
+  const int64_t ntiles = (acc->vocab + sv::kLmhNT - 1) / sv::kLmhNT;
+  off_tiles = P.device_bytes;
+  device_bytes = align_up(off_tiles + sizeof(sv::ChunkStat) * (size_t)(P.Nq * ntiles));
+  return SPEC_OK;
+}
 
 spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, const spec_accept_args_t* acc,
                   void* ws, size_t ws_bytes, void* staging, size_t staging_bytes, void* stream,
@@ -587,6 +616,7 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     c.nodes = reinterpret_cast<sv::NodeInfo*>(d + P.off_acc_nodes);
     c.per_req = P.per_req ? 1 : 0;
     c.nodes_n16 = (int32_t)((sizeof(sv::NodeInfo) * P.nodes.size() + 15) / 16);
+    c.all_stats = (P.per_req || mode.lm) ? 1 : 0;
   }
 
   // Optional device check of the acceptance inputs (the caller's contract),
@@ -598,6 +628,35 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     if (hipMemcpyAsync(&hflag, dflag, sizeof(hflag), hipMemcpyDeviceToHost, s) != hipSuccess) return SPEC_ERR_HIP;
     if (hipStreamSynchronize(s) != hipSuccess) return SPEC_ERR_HIP;
     if (hflag != 0) return SPEC_ERR_INVALID_ARG;
+  }
+
+  if (mode.lm) {
+    // the LM head, then its tile statistics folded into chunk statistics,
+    // then the decision and final sample, all on the caller's stream
+    const spec_lm_head_args_t* lm = mode.lm;
+    sv::LmhParams g{};
+    g.hidden = static_cast<const uint16_t*>(lm->hidden);
+    g.weight = static_cast<const uint16_t*>(lm->weight);
+    g.h_st = lm->hidden_stride;
+    g.w_st = lm->weight_stride;
+    g.out = const_cast<void*>(acc->target_logits);
+    g.o_st = acc->logits_stride;
+    g.tiles = reinterpret_cast<sv::ChunkStat*>(d + mode.off_tiles);
+    g.M = (int32_t)P.Nq;
+    g.K = lm->hidden_dim;
+    g.V = acc->vocab;
+    g.ntiles = (acc->vocab + sv::kLmhNT - 1) / sv::kLmhNT;
+    g.m_tiles = (g.M + 16 * sv::lmh_row_blocks(g.M) - 1) / (16 * sv::lmh_row_blocks(g.M));
+    g.out_bf16 = acc->dtype == SPEC_BF16;
+    if (lm->event_begin && hipEventRecord(static_cast<hipEvent_t>(lm->event_begin), s) != hipSuccess) return SPEC_ERR_HIP;
+    if (sv::launch_lmh(g, s) != hipSuccess) return SPEC_ERR_HIP;
+    if (lm->event_end && hipEventRecord(static_cast<hipEvent_t>(lm->event_end), s) != hipSuccess) return SPEC_ERR_HIP;
+    if (acc->event_begin && hipEventRecord(static_cast<hipEvent_t>(acc->event_begin), s) != hipSuccess) return SPEC_ERR_HIP;
+    if (sv::launch_foldstats(c, g.tiles, g.ntiles, s) != hipSuccess) return SPEC_ERR_HIP;
+    if (acc->event_mid && hipEventRecord(static_cast<hipEvent_t>(acc->event_mid), s) != hipSuccess) return SPEC_ERR_HIP;
+    if (sv::launch_decide(c, s) != hipSuccess) return SPEC_ERR_HIP;
+    if (acc->event_end && hipEventRecord(static_cast<hipEvent_t>(acc->event_end), s) != hipSuccess) return SPEC_ERR_HIP;
+    return SPEC_OK;
   }
 
   auto launch_acc = [&](hipStream_t st) -> bool {
@@ -692,6 +751,33 @@ spec_status_t spec_verify_noalloc(const spec_requests_t* req, const spec_attn_ar
   mode.pageable = true;
   mode.staging_mu = &staging_mu;
   return run(req, attn, acc, scratch, sv::kNoAllocScratchBytes, host_staging, sizeof(host_staging), stream, mode);
+}
+
+spec_status_t spec_lm_head_workspace_bytes(const spec_requests_t* req, const spec_lm_head_args_t* lm,
+                                           const spec_accept_args_t* acc, size_t* device_bytes, size_t* host_bytes) {
+  if (!device_bytes || !host_bytes) return SPEC_ERR_INVALID_ARG;
+  Plan P;
+  size_t off = 0, dev = 0;
+  const spec_status_t st = lm_plan(req, lm, acc, P, off, dev);
+  if (st != SPEC_OK) return st;
+  *device_bytes = dev;
+  *host_bytes = P.plan_bytes;
+  return SPEC_OK;
+}
+
+spec_status_t spec_lm_head_accept(const spec_requests_t* req, const spec_lm_head_args_t* lm,
+                                  const spec_accept_args_t* acc, void* workspace, size_t workspace_bytes,
+                                  void* host_staging, size_t host_staging_bytes, void* stream) {
+  Plan P;
+  size_t off = 0, dev = 0;
+  const spec_status_t st = lm_plan(req, lm, acc, P, off, dev);
+  if (st != SPEC_OK) return st;
+  if (workspace_bytes < dev) return SPEC_ERR_WORKSPACE;
+  RunMode mode;
+  mode.overlap = false;
+  mode.lm = lm;
+  mode.off_tiles = off;
+  return run(req, nullptr, acc, workspace, workspace_bytes, host_staging, host_staging_bytes, stream, mode);
 }
 
 const char* spec_status_str(spec_status_t status) {

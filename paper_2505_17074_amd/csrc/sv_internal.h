@@ -151,9 +151,46 @@ struct AccParams {
   NodeInfo* nodes;
   int32_t per_req;
   int32_t nodes_n16;
+  int32_t all_stats;   // every row has chunk statistics before the decision kernel runs
+  int32_t pad1;
 };
 
 constexpr int kAccMaxChunks = 1024;    // vocabularies up to 4M entries
+
+// The target model's LM head, logits = hidden . weight^T, with the softmax
+// statistics of each (row, kLmhNT-entry tile) taken in the epilogue.
+constexpr int kLmhNT = 256;            // vocabulary entries per work-group and statistics tile
+constexpr int kLmhTilesPerChunk = kAccChunk / kLmhNT;
+struct LmhParams {
+  const uint16_t* hidden;   // [M, K] bf16, row stride h_st elements
+  const uint16_t* weight;   // [V, K] bf16, row stride w_st elements
+  int64_t h_st, w_st;
+  void* out;                // [M, V] logits (fp32, or bf16 when out_bf16), row stride o_st elements
+  int64_t o_st;
+  ChunkStat* tiles;         // [M, ntiles] per-tile (sum of exp(l - max), max)
+  int32_t M, K, V, ntiles;
+  int32_t m_tiles;          // row tiles of 16 * MB rows
+  int32_t out_bf16;
+};
+// Rows per row tile (in units of 16) for M rows: the fewest tiles of at most
+// 128 rows, each as small as the split allows.
+int lmh_row_blocks(int M);
+hipError_t launch_lmh(const LmhParams& p, hipStream_t s);
+// Chunk statistics [Nq, nch] (the decision kernel's input) folded from the
+// LM head's tile statistics, plus the row-statistics kernel's other duties
+// (the request and node tables' device copies, cleared tickets).
+hipError_t launch_foldstats(const AccParams& p, const ChunkStat* tiles, int ntiles, hipStream_t s);
+
+// exp(x - m) for x <= m (a logit against a maximum): the hardware base-2
+// exponential of (x - m) log2 e.  Its error is about an ulp of the result
+// plus the roundings of x - m and of the product, the same order as the
+// library expf, in three instructions instead of a dozen.  Every kernel that
+// takes softmax statistics of logits evaluates exp(l - m) through this one
+// function, so a statistic and the entries it summarises are always computed
+// alike.
+__device__ __forceinline__ float exp_rel(float x, float m) {
+  return __builtin_amdgcn_exp2f((x - m) * 1.4426950408889634f);
+}
 
 // Largest number of query rows (heads x verify positions) one work item holds.
 int max_rows_per_item(int dtype_bf16, int D);

@@ -147,6 +147,8 @@ class Pool:
     draft_tokens: np.ndarray     # int32 [Nq - B]
     uniforms: np.ndarray         # float32 [Nq]
     tree_parents: Optional[list] = None   # per request, its own BFS parent array (instead of tree_parent)
+    hidden: Optional[np.ndarray] = None   # LM-head inputs (make_lm_head_pool): [Nq, K] bf16 bits
+    weight: Optional[np.ndarray] = None   # [V, K] bf16 bits
 
     @property
     def batch(self) -> int:
@@ -405,3 +407,71 @@ def accept_bytes_read(pool: Pool, accepted_node: np.ndarray) -> int:
         rows = Nq
         qrows = int((node < pool.draft_len).sum())
     return int((rows + qrows) * V * s_l + (Nq - B) * (4 + s_l) + Nq * 4 + 8 * B)
+
+
+# hidden size of the target model behind each workload (LLaMA-7B-like 4096;
+# the 64-head long-context model 8192)
+LM_HIDDEN = {"tiny_f32": 256, "mha7b_b32": 4096, "ragged_gqa_b128": 4096, "long_gqa_b8": 8192, "tree15_b64": 4096}
+
+
+def make_lm_head_pool(cfg: Config, seed: int = 0, batch: Optional[int] = None,
+                      hidden_dim: Optional[int] = None, vocab: Optional[int] = None) -> Pool:
+    """A workload's acceptance inputs with the target logits left to the LM
+    head: the verify positions' final hidden states [Nq, K] ~ N(0, 1) and the
+    LM head's weights [V, K] ~ N(0, 4 / K), both stored in bf16, so that the
+    logits have a standard deviation of about 2 (the draft-logit scale of
+    make_pool).  The draft model is emulated as an LM head of its own over
+    the same hidden states, weights W + N(0, 1 / K) (the target's plus noise),
+    plus N(0, sigma_i^2) on its logits with the workload's per-request sigma;
+    its distributions are stored in the logit dtype and the draft tokens
+    drawn from them.  Q, K and V are not drawn (empty); target_logits is a
+    zero buffer of the right shape for the LM head to fill.  Draw order:
+    request scalars, hidden states, weights, draft-weight noise (by blocks of
+    8192 vocabulary rows), draft-logit noise, draft tokens, uniforms."""
+    if batch is not None:
+        cfg = dataclasses.replace(cfg, batch=int(batch))
+    if vocab is not None:
+        cfg = dataclasses.replace(cfg, vocab=int(vocab))
+    K = int(hidden_dim or LM_HIDDEN.get(cfg.name, 4096))
+    rng = _rng(cfg, seed)
+    B, V = cfg.batch, cfg.vocab
+    ctx, klen, sigma = _draw_request_scalars(rng, cfg)
+    parent = full_binary_tree_parents(cfg.draft[1], cfg.draft[2]) if cfg.is_tree else None
+    n_q = np.full(B, len(parent), np.int64) if parent is not None else klen.astype(np.int64) + 1
+    Nq = int(n_q.sum())
+    hidden = storage(rng.standard_normal((Nq, K), dtype=np.float32), BF16)
+    weight = storage(rng.standard_normal((V, K), dtype=np.float32) * np.float32(2.0 / math.sqrt(K)), BF16)
+    q_start = np.concatenate([[0], np.cumsum(n_q)])
+    if parent is None:
+        internal_local = [np.arange(int(kk)) for kk in klen]
+    else:
+        internal = sorted(set(int(p) for p in parent[1:]))
+        internal_local = [np.array(internal)] * B
+    rows = np.concatenate([q_start[i] + internal_local[i] for i in range(B)]).astype(np.int64) \
+        if B else np.zeros(0, np.int64)
+    Hr = bf16_bits_to_f32(hidden[rows]) if rows.size else np.zeros((0, K), np.float32)
+    z = np.zeros((rows.size, V), np.float32)
+    for v0 in range(0, V, 8192):
+        wb = bf16_bits_to_f32(weight[v0:v0 + 8192])
+        wb = wb + rng.standard_normal(wb.shape, dtype=np.float32) * np.float32(1.0 / math.sqrt(K))
+        z[:, v0:v0 + 8192] = Hr @ wb.T
+    req_of_row = np.repeat(np.arange(B), [len(x) for x in internal_local])
+    z = z.astype(np.float64) + rng.standard_normal(z.shape) * sigma[req_of_row][:, None]
+    draft_probs = storage(_softmax_rows(z).astype(np.float32), cfg.logit_dtype) if rows.size \
+        else np.zeros((0, V), np.uint16 if cfg.logit_dtype == BF16 else np.float32)
+    stored = as_f32(draft_probs, cfg.logit_dtype).astype(np.float64)
+    d_start = np.concatenate([[0], np.cumsum([len(x) for x in internal_local])])
+    src_rows = []
+    for i in range(B):
+        par_local = np.arange(int(n_q[i]) - 1) if parent is None else parent[1:]
+        rank = {int(n): r for r, n in enumerate(internal_local[i])}
+        src_rows.extend(int(d_start[i]) + rank[int(p)] for p in par_local)
+    src_rows = np.asarray(src_rows, dtype=np.int64)
+    draft_tokens = _categorical(rng, stored[src_rows]) if src_rows.size else np.zeros(0, np.int32)
+    uniforms = (rng.integers(0, 1 << 24, size=Nq).astype(np.float64) * 2.0 ** -24).astype(np.float32)
+    empty = np.zeros((0, cfg.num_q_heads, cfg.head_dim), np.float32)
+    empty_kv = np.zeros((0, cfg.num_kv_heads, cfg.head_dim), np.float32)
+    target = np.zeros((Nq, V), np.uint16 if cfg.logit_dtype == BF16 else np.float32)
+    return Pool(cfg, seed, ctx, klen, parent, sigma, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim,
+                cfg.qkv_dtype, cfg.logit_dtype, V, empty, empty_kv, empty_kv, target, draft_probs,
+                draft_tokens, uniforms, hidden=hidden, weight=weight)

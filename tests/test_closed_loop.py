@@ -53,3 +53,26 @@ def test_gpu_traces_match_the_oracle(gpu_lib):
     assert ok.all()
     res = CL.evaluate(CL.requests_from(cfg, wl, traces), CL.default_params(cfg))
     assert all(r["avg_latency_ms"] > 0 for r in res.values())
+
+
+def test_round_time_includes_the_measured_verify_kernels():
+    """A request's round is n * T_SSM + T_LLM plus the verify kernels' time
+    interpolated at its context (prompt plus half its output)."""
+    cfg = CL.LoopConfig(requests=5, verify_us={128: 300.0, 2048: 1100.0})
+    wl = CL.make_workload(cfg, 2)
+    R = int(wl.out_len.max())
+    reqs = CL.requests_from(cfg, wl, np.zeros((cfg.requests, R), np.int64))
+    for i, r in enumerate(reqs):
+        c = float(wl.prompt[i]) + wl.out_len[i] / 2
+        extra = np.interp(c, [128, 2048], [300.0, 1100.0])
+        assert r.round_us == cfg.draft * cfg.t_ssm_us + cfg.t_llm_us + int(round(extra))
+    base = CL.requests_from(CL.LoopConfig(requests=5), wl, np.zeros((5, R), np.int64))
+    assert all(b.round_us == cfg.draft * cfg.t_ssm_us + cfg.t_llm_us for b in base)
+
+
+@pytest.mark.gpu
+def test_measured_verify_times(gpu_lib):
+    print("[case] closed-loop verify-kernel times", flush=True)
+    t = CL.measure_verify("cuda", contexts=(128, 2048), reps=5)
+    assert set(t) == {128, 2048} and all(np.isfinite(v) and v > 0 for v in t.values())
+    assert t[2048] > t[128]            # 32 layers' attention over 16x the keys
