@@ -42,6 +42,7 @@ def parse():
     ap.add_argument("--no-sched", action="store_true",
                     help="skip the scheduler's closed loop (thousands of small launches; for profiler runs)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-lm-head", action="store_true", help="skip the fused LM-head figures")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only copy BYTES device-to-device three times (the calibration run for the "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -127,7 +128,8 @@ def scheduler_closed_loop(dev, seed: int) -> dict:
     from paper_2505_17074_amd import closed_loop as CL
     from paper_2505_17074_amd.scheduler import simulate
     swap = CL.measure_swap(dev)
-    cfg = CL.LoopConfig(swap_us_per_token=swap["us_per_token"])
+    verify = CL.measure_verify(dev)
+    cfg = CL.LoopConfig(swap_us_per_token=swap["us_per_token"], verify_us=verify)
     wl = CL.make_workload(cfg, seed)
     t0 = time.perf_counter()
     traces = CL.gpu_traces(cfg, wl, seed, device=dev)
@@ -143,7 +145,9 @@ def scheduler_closed_loop(dev, seed: int) -> dict:
     return {"workload": f"{cfg.requests} requests, draft {cfg.draft}, output lengths log-normal (median "
                         f"{cfg.out_median}), predicted with log-normal error sigma {cfg.pred_sigma}, per-request "
                         f"acceptance from target noise sigma in {list(cfg.sigma)}; rounds "
-                        f"{cfg.draft} x {cfg.t_ssm_us} + {cfg.t_llm_us} us; KV swap {cfg.swap_us_per_token} us/token",
+                        f"{cfg.draft} x {cfg.t_ssm_us} + {cfg.t_llm_us} us + the measured verify kernels (32 layers' "
+                        f"attention + acceptance) at the request's context; KV swap {cfg.swap_us_per_token} us/token",
+            "verify_us_by_context": verify,
             "rounds_traced": int(traces.shape[1]), "trace_s": t_traces,
             "mean_tokens_per_round": float((traces + 1).mean()),
             "avg_latency_ms": lat,
@@ -242,6 +246,72 @@ def cpu_baseline(pool, budget_s: float):
             "kind": "oracle",
             "sample": f"{m} request verifications ({m / pool.batch:.2f} passes over the {pool.batch} requests, "
                       f"{done_tokens} verify tokens), attention + acceptance in fp64 NumPy, {t_used:.1f} s"}
+
+
+def lm_head_figures(name: str, seed: int, dev, flush, reps: int = 10) -> dict:
+    """The LM head fused with acceptance (spec_lm_head_accept) on the
+    workload's verify positions: the GEMM's time (events around its kernel,
+    after a cache flush), its MFMA and HBM rooflines, torch's bf16 linear
+    (hipBLASLt) on the same tensors as a reference point, and the fused
+    acceptance (statistics fold + decision) beside the unfused one (row pass
+    + decision) on the same logits."""
+    import numpy as np
+    import torch
+    from paper_2505_17074_amd import binding as B
+    from paper_2505_17074_amd import workload as W
+    from paper_2505_17074_amd.batch import LmHeadVerifier
+    print(f"[bench] {name}: LM head", file=sys.stderr, flush=True)
+    pool = W.make_lm_head_pool(W.CONFIG_BY_NAME[name], seed)
+    lmv = LmHeadVerifier(pool, dev)
+    M, K = pool.hidden.shape
+    V = pool.vocab
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    for e in ev:
+        e.record()
+    torch.cuda.synchronize()
+    lmv.lm.event_begin, lmv.lm.event_end = ev[0].cuda_event, ev[1].cuda_event
+    lmv.acc.event_begin, lmv.acc.event_end = ev[2].cuda_event, ev[3].cuda_event
+    g, a, t = [], [], []
+    for rep in range(reps + 2):
+        flush()
+        lmv.run()
+        torch.cuda.synchronize()
+        g.append(ev[0].elapsed_time(ev[1]) * 1e3)
+        a.append(ev[2].elapsed_time(ev[3]) * 1e3)
+    for rep in range(reps + 2):
+        flush()
+        ev[4].record()
+        y = torch.nn.functional.linear(lmv.hidden, lmv.weight)
+        ev[5].record()
+        torch.cuda.synchronize()
+        t.append(ev[4].elapsed_time(ev[5]) * 1e3)
+    del y
+    # the unfused acceptance on the logits the GEMM wrote
+    b = lmv.batch
+    req, acc = b.requests(), b.accept_args()
+    st, db, hb = B.spec_workspace_bytes(req, None, acc)
+    B.check(st, "spec_workspace_bytes")
+    ws = torch.empty(db + 256, dtype=torch.uint8, device=dev)
+    stg = torch.empty(max(hb, 1), dtype=torch.uint8, pin_memory=True)
+    acc.event_begin, acc.event_end = ev[2].cuda_event, ev[3].cuda_event
+    u = []
+    for rep in range(reps + 2):
+        flush()
+        B.check(B.spec_accept(req, acc, (ws.data_ptr() + 255) // 256 * 256, db, stg.data_ptr(), hb,
+                              torch.cuda.current_stream(dev).cuda_stream), "spec_accept")
+        torch.cuda.synchronize()
+        u.append(ev[2].elapsed_time(ev[3]) * 1e3)
+    gem, tor = float(np.median(g[2:])), float(np.median(t[2:]))
+    flops = 2.0 * M * K * V
+    nbytes = V * K * 2 + M * K * 2 + M * V * (2 if pool.logit_dtype == W.BF16 else 4)
+    out = {"rows": int(M), "hidden_dim": int(K), "vocab": int(V), "logits": pool.logit_dtype,
+           "gemm_us": gem, "tflops": flops / gem / 1e6, "mfma_frac": flops / (gem * 1e-6) / MFMA_BF16_PEAK,
+           "bytes": int(nbytes), "hbm_frac": nbytes / (gem * 1e-6) / 1e9 / HBM_PEAK_GBS,
+           "torch_linear_bf16_us": tor,
+           "accept_fused_us": float(np.median(a[2:])), "accept_unfused_us": float(np.median(u[2:]))}
+    del lmv, b, ws
+    torch.cuda.empty_cache()
+    return out
 
 
 HEADLINE = "ragged_gqa_b128"          # the largest workload that fits one GPU
@@ -498,6 +568,9 @@ def main():
         if name == args.workload:
             head_pool = pool
         del pool, res
+    if not args.no_lm_head:
+        for name in names:
+            figs[name]["lm_head"] = lm_head_figures(name, args.seed, dev, flush)
     del flush
     head = figs[args.workload]
     # the device's stream ceilings last: their 20 ms of full-rate reads and
@@ -528,6 +601,7 @@ def main():
                  "stay in the Infinity Cache); cold: each step after a cache flush",
         "cold": head["cold"],
         "accept": head["accept"],
+        "lm_head": head.get("lm_head"),
         # the other workloads, measured the same way in the same run
         "workloads": {n: f for n, f in figs.items() if n != args.workload},
     }

@@ -29,8 +29,16 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-constexpr int kLmhThreads = 256;
 constexpr int kRowB = 64;            // bytes of one 32-k row slice in LDS
+#ifndef SV_LMH_WAVES
+#define SV_LMH_WAVES 8
+#endif
+#ifndef SV_LMH_MAXROWS
+#define SV_LMH_MAXROWS 128
+#endif
+constexpr int kLmhWaves = SV_LMH_WAVES;   // waves per work-group
+constexpr int kLmhThreads = 64 * kLmhWaves;
+constexpr int kLmhCB = kLmhNT / (16 * kLmhWaves);   // 16-column blocks per wave
 
 template <int N>
 __device__ __forceinline__ void lmh_wait_vm() {
@@ -50,14 +58,16 @@ struct LmhGeo {
   static constexpr int ROWS = RA + kLmhNT;            // LDS rows per stage
   static constexpr int STAGE = ROWS * kRowB;
   static constexpr int XF = ROWS / 16;                // 1 KB transfers per stage (16 rows each)
-  static constexpr int PER = (XF + 3) / 4;            // per wave (padded with repeats)
+  static constexpr int PER = (XF + kLmhWaves - 1) / kLmhWaves;   // per wave (padded with repeats)
 };
 
 // Ring depth by row blocks: weight-streaming shapes (few rows) keep more
 // stages in flight; the LDS also holds the epilogue's reductions.
 template <int MB>
 struct LmhStages {
-  static constexpr int value = MB <= 5 ? 6 : 4;
+  // as many stages as 144 KB of LDS holds, at most 6
+  static constexpr int fit = (144 * 1024) / LmhGeo<MB>::STAGE;
+  static constexpr int value = fit < 6 ? fit : 6;
 };
 
 template <int MB, int NS, bool BF16OUT>
@@ -92,7 +102,7 @@ __global__ __launch_bounds__(kLmhThreads) void lmh_gemm(LmhParams p) {
   int dst[PER];
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
-    const int j = (w + 4 * q) % G::XF;               // transfer index (repeats pad the last wave)
+    const int j = (w + kLmhWaves * q) % G::XF;       // transfer index (repeats pad the last wave)
     const int row = 16 * j + lane / 4;               // LDS row of this lane's chunk
     const int chunk = (lane & 3) ^ lmh_swz(row);     // global chunk that lands at LDS chunk lane & 3
     isw[q] = row >= G::RA;
@@ -109,21 +119,22 @@ __global__ __launch_bounds__(kLmhThreads) void lmh_gemm(LmhParams p) {
                                                0);
   };
 
-  f32x4 acc[MB][4];
+  constexpr int CB = kLmhCB;
+  f32x4 acc[MB][CB];
 #pragma unroll
   for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int cb = 0; cb < CB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
   // LDS read offsets (stage 0) of this lane's A rows and B rows
-  uint32_t aoff[MB], boff[4];
+  uint32_t aoff[MB], boff[CB];
 #pragma unroll
   for (int rb = 0; rb < MB; ++rb) {
     const int row = 16 * rb + l16;
     aoff[rb] = row * kRowB + ((grp ^ lmh_swz(row)) * 16);
   }
 #pragma unroll
-  for (int cb = 0; cb < 4; ++cb) {
-    const int row = G::RA + 64 * w + 16 * cb + l16;
+  for (int cb = 0; cb < CB; ++cb) {
+    const int row = G::RA + 16 * CB * w + 16 * cb + l16;
     boff[cb] = row * kRowB + ((grp ^ lmh_swz(row)) * 16);
   }
 
@@ -139,14 +150,14 @@ __global__ __launch_bounds__(kLmhThreads) void lmh_gemm(LmhParams p) {
     lmh_barrier();                  // everyone's have; stage (t - 1) % NS is free
     if (t + NS - 1 < nk) issue((t + NS - 1) % NS, t + NS - 1);
     const char* sb = lds + stage * G::STAGE;
-    bf16x8 bop[4];
+    bf16x8 bop[CB];
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) bop[cb] = *reinterpret_cast<const bf16x8*>(sb + boff[cb]);
+    for (int cb = 0; cb < CB; ++cb) bop[cb] = *reinterpret_cast<const bf16x8*>(sb + boff[cb]);
 #pragma unroll
     for (int rb = 0; rb < MB; ++rb) {
       const bf16x8 aop = *reinterpret_cast<const bf16x8*>(sb + aoff[rb]);
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, bop[cb], acc[rb][cb], 0, 0, 0);
+      for (int cb = 0; cb < CB; ++cb) acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, bop[cb], acc[rb][cb], 0, 0, 0);
     }
   }
   lmh_wait_vm<0>();
@@ -157,14 +168,15 @@ __global__ __launch_bounds__(kLmhThreads) void lmh_gemm(LmhParams p) {
   // stored values: the maximum, then the sum of exp(l - max) in fp64, lane
   // sums in column-block order, then across the 16 lanes of a row by an xor
   // butterfly, then across the four waves in wave order.
-  float* red_m = reinterpret_cast<float*>(lds);                    // [4][RA]
-  double* red_s = reinterpret_cast<double*>(lds + 4 * G::RA * 4);  // [4][RA]
-  float val[MB][4][4];
+  constexpr int NW = kLmhWaves;
+  float* red_m = reinterpret_cast<float*>(lds);                     // [NW][RA]
+  double* red_s = reinterpret_cast<double*>(lds + NW * G::RA * 4);  // [NW][RA]
+  float val[MB][CB][4];
 #pragma unroll
   for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < 4; ++cb) {
-      const int col = 64 * w + 16 * cb + l16;
+    for (int cb = 0; cb < CB; ++cb) {
+      const int col = 16 * CB * w + 16 * cb + l16;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 16 * rb + 4 * grp + i;
@@ -185,28 +197,37 @@ __global__ __launch_bounds__(kLmhThreads) void lmh_gemm(LmhParams p) {
   for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float m = fmaxf(fmaxf(val[rb][0][i], val[rb][1][i]), fmaxf(val[rb][2][i], val[rb][3][i]));
+      float m = val[rb][0][i];
+#pragma unroll
+      for (int cb = 1; cb < CB; ++cb) m = fmaxf(m, val[rb][cb][i]);
       for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o));
       if (l16 == 0) red_m[w * G::RA + 16 * rb + 4 * grp + i] = m;
     }
   __syncthreads();
+  auto row_max = [&](int row) {
+    float m = red_m[row];
+#pragma unroll
+    for (int x = 1; x < NW; ++x) m = fmaxf(m, red_m[x * G::RA + row]);
+    return m;
+  };
 #pragma unroll
   for (int rb = 0; rb < MB; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = 16 * rb + 4 * grp + i;
-      const float m = fmaxf(fmaxf(red_m[row], red_m[G::RA + row]), fmaxf(red_m[2 * G::RA + row], red_m[3 * G::RA + row]));
+      const float m = row_max(row);
       double sm = 0.0;
 #pragma unroll
-      for (int cb = 0; cb < 4; ++cb) sm += (double)exp_rel(val[rb][cb][i], m);
+      for (int cb = 0; cb < CB; ++cb) sm += (double)exp_rel(val[rb][cb][i], m);
       for (int o = 1; o < 16; o <<= 1) sm += __shfl_xor(sm, o);
       if (l16 == 0) red_s[w * G::RA + row] = sm;
     }
   __syncthreads();
   for (int row = threadIdx.x; row < mrows; row += kLmhThreads) {
-    const float m = fmaxf(fmaxf(red_m[row], red_m[G::RA + row]), fmaxf(red_m[2 * G::RA + row], red_m[3 * G::RA + row]));
-    const double sm = ((red_s[row] + red_s[G::RA + row]) + red_s[2 * G::RA + row]) + red_s[3 * G::RA + row];
-    p.tiles[(int64_t)(m0 + row) * p.ntiles + nt] = ChunkStat{sm, m, 0.f};
+    double sm = red_s[row];
+#pragma unroll
+    for (int x = 1; x < NW; ++x) sm += red_s[x * G::RA + row];
+    p.tiles[(int64_t)(m0 + row) * p.ntiles + nt] = ChunkStat{sm, row_max(row), 0.f};
   }
 #endif
 }
@@ -224,7 +245,7 @@ hipError_t launch_mb(const LmhParams& p, hipStream_t s) {
 }  // namespace
 
 int lmh_row_blocks(int M) {
-  const int tiles = (M + 127) / 128;
+  const int tiles = (M + SV_LMH_MAXROWS - 1) / SV_LMH_MAXROWS;
   const int rows = (M + tiles - 1) / tiles;
   return (rows + 15) / 16;
 }
@@ -239,6 +260,10 @@ hipError_t launch_lmh(const LmhParams& p, hipStream_t s) {
     case 6: return launch_mb<6>(p, s);
     case 7: return launch_mb<7>(p, s);
     case 8: return launch_mb<8>(p, s);
+#if SV_LMH_MAXROWS > 128
+    case 9: return launch_mb<9>(p, s);
+    case 10: return launch_mb<10>(p, s);
+#endif
     default: return hipErrorInvalidValue;
   }
 }
