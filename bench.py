@@ -43,6 +43,8 @@ def parse():
                     help="skip the scheduler's closed loop (thousands of small launches; for profiler runs)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-lm-head", action="store_true", help="skip the fused LM-head figures")
+    ap.add_argument("--settle", type=float, default=0.3, metavar="SECONDS",
+                    help="untimed steps for this long before the warm-up steps, while the clocks ramp")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only copy BYTES device-to-device three times (the calibration run for the "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -318,7 +320,7 @@ HEADLINE = "ragged_gqa_b128"          # the largest workload that fits one GPU
 OTHERS = ("mha7b_b32", "long_gqa_b8", "tree15_b64")
 
 
-def measure_workload(name: str, seed: int, K: int, Wm: int, dev, flush) -> tuple:
+def measure_workload(name: str, seed: int, K: int, Wm: int, dev, flush, settle_s: float = 0.3) -> tuple:
     """Every GPU figure of one workload: warm and cold steps, the attention
     kernels alone (split + combine, packed and paged), the acceptance
     kernels alone (cold and warm; the row-statistics kernel alone; the
@@ -345,6 +347,15 @@ def measure_workload(name: str, seed: int, K: int, Wm: int, dev, flush) -> tuple
             e.record(stream)          # materialise the events
     torch.cuda.synchronize()
 
+    # Clocks settle first: the GPU's clocks ramp over the first tens of
+    # milliseconds of work, so untimed steps run for `settle_s` of wall time
+    # before the W warm-up steps (neither is timed; the timed region below is
+    # exactly K steps).
+    t_end = time.perf_counter() + settle_s
+    while time.perf_counter() < t_end:
+        for _ in range(20):
+            ver.run("verify", stream)
+        torch.cuda.synchronize()
     for _ in range(Wm):
         ver.run("verify", stream)
     torch.cuda.synchronize()
@@ -560,7 +571,7 @@ def main():
     names = [args.workload] + ([] if args.only else [n for n in OTHERS + (HEADLINE,) if n != args.workload])
     figs, checks, head_pool = {}, {}, None
     for name in names:
-        fig, pool, res = measure_workload(name, args.seed, args.steps, args.warmup, dev, flush)
+        fig, pool, res = measure_workload(name, args.seed, args.steps, args.warmup, dev, flush, args.settle)
         figs[name] = fig
         if not args.no_cpu:
             # the cpu_baseline leg: the oracle's verdict on this step's outputs

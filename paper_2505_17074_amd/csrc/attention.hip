@@ -99,6 +99,9 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 #ifndef SV_NS_W4
 #define SV_NS_W4 3
 #endif
+#ifndef SV_WPE_W5
+#define SV_WPE_W5 4
+#endif
 #ifndef SV_NS_W5
 #define SV_NS_W5 3
 #endif
@@ -349,7 +352,7 @@ struct AttnLds {
 // 3-4 waves to 168 (three work-groups per compute unit) measured neutral.
 template <int W>
 struct WavesPerEu {
-  static constexpr int value = W == 5 ? 4 : (W >= 3 ? SV_WPE_W34 : 1);
+  static constexpr int value = W == 5 ? SV_WPE_W5 : (W >= 3 ? SV_WPE_W34 : 1);
 };
 
 // PG: paged KV cache.  A tile (32 keys, 32-aligned) never straddles a page

@@ -163,7 +163,10 @@ int device_cus() {
 // items on 256 compute units) every width, at d = 64 and d = 128, runs 7-27%
 // faster than with 9 pieces each (576 items), whose last 64 items form a
 // second, nearly empty round.
-int groups_per_cu(int /*waves*/) { return 2; }
+#ifndef SV_GROUPS_W5
+#define SV_GROUPS_W5 2
+#endif
+int groups_per_cu(int waves) { return waves == 5 ? SV_GROUPS_W5 : 2; }
 
 // Piece length for a stream of L >= 1 keys and a split of s >= 1 keys: the
 // stream cut into ceil(L / s) equal parts, rounded up to 32 keys (a short
@@ -172,11 +175,6 @@ int groups_per_cu(int /*waves*/) { return 2; }
 int piece_len(int L, int64_t s) {
   const int64_t n0 = (L + s - 1) / s;
   return (int)(((L + n0 - 1) / n0 + 31) / 32 * 32);
-}
-// Pieces of that length covering the stream; non-increasing in s.
-int pieces_for(int L, int64_t s) {
-  const int piece = piece_len(L, s);
-  return (L + piece - 1) / piece;
 }
 
 // Keys per split piece.  `slots` = work-groups the device runs at once;
@@ -194,34 +192,66 @@ int pieces_for(int L, int64_t s) {
 //    for a second round (on 8 requests of 16K-32K keys x 8 KV heads, 504 items
 //    of <= 3264 keys: about 7% faster than 408 items of <= 4096 keys, and 24%
 //    faster than 528 items of <= 3072).
-constexpr int64_t kMaxPiece = 4096;
+#ifndef SV_MAX_PIECE
+#define SV_MAX_PIECE 4096
+#endif
+constexpr int64_t kMaxPiece = SV_MAX_PIECE;
 constexpr int64_t kMaxSplit = 1 << 20;
-int auto_split(const std::vector<int>& len, const std::vector<int>& mult, int rows_max, int64_t slots) {
+// Keys per piece of each request's streams (every KV head and head group of
+// a request has the same length).  `slots` = work-groups the device runs at
+// once; `len[i]` = keys of request i, each the length of `mult[i]` streams.
+// Pieces stay >= 40 * rows keys, so the fp32 partials (rows x d x 4 bytes,
+// written once and read once by the combine) remain a few percent of the K/V
+// bytes a piece streams (32 rows x d x 2 x 2 per 32 keys), and >= 256 keys.
+//  - At least as many streams as slots: pieces of at most kMaxPiece keys,
+//    dispatched longest first.  A longer item, started first, still outlasts
+//    the rest of the kernel once the other work-groups have drained (measured
+//    on ragged batches: 6464-key pieces 28% slower than 4096; 2048 and 3072
+//    were 4% and 2% slower than 4096).
+//  - Fewer streams than slots: every work-group takes exactly one item (a
+//    second, nearly empty round of items ran 7-27% slower), and the pieces
+//    are cut so that the longest is as short as the slots allow: one piece
+//    per stream to start with, then repeatedly one more piece for the
+//    request whose pieces are currently longest, while its streams' extra
+//    items still fit the slots.  Every work-group streams at about the same
+//    rate, so the longest piece sets the kernel's end.
+std::vector<int> piece_lengths(const std::vector<int>& len, const std::vector<int>& mult, int rows_max, int64_t slots) {
   slots = std::max<int64_t>(slots, 1);
   int64_t lo = std::max<int64_t>(40 * (int64_t)rows_max, 256);
   lo = std::min<int64_t>((lo + 31) / 32 * 32, kMaxSplit);
+  const size_t B = len.size();
+  std::vector<int> out(B);
   int64_t streams = 0;
-  int max_len = 1;
-  for (size_t i = 0; i < len.size(); ++i) {
-    streams += mult[i];
-    max_len = std::max(max_len, len[i]);
+  for (size_t i = 0; i < B; ++i) streams += mult[i];
+  if (streams >= slots) {
+    for (size_t i = 0; i < B; ++i) out[i] = piece_len(len[i], std::max(kMaxPiece, lo));
+    return out;
   }
-  if (streams >= slots) return (int)std::max(kMaxPiece, lo);
-  auto items = [&](int64_t s) {
-    int64_t n = 0;
-    for (size_t i = 0; i < len.size(); ++i) n += (int64_t)pieces_for(len[i], s) * mult[i];
-    return n;
-  };
-  // items() is non-increasing in s; items(hi) = streams < slots unless a
-  // request is longer than kMaxSplit keys
-  const int64_t hi = std::max(lo, std::min<int64_t>(((int64_t)max_len + 31) / 32 * 32, kMaxSplit));
-  if (items(lo) <= slots || items(hi) > slots) return (int)(items(lo) <= slots ? lo : hi);
-  int64_t a = lo / 32, b = hi / 32;        // items(32 a) > slots >= items(32 b)
-  while (b - a > 1) {
-    const int64_t m = (a + b) / 2;
-    if (items(32 * m) <= slots) b = m; else a = m;
+  // greedy: a max-heap of (current piece length, request)
+  std::vector<int64_t> n(B, 1);
+  auto cur = [&](size_t i) { return ((int64_t)len[i] + n[i] - 1) / n[i]; };
+  std::vector<std::pair<int64_t, size_t>> heap;
+  heap.reserve(B);
+  for (size_t i = 0; i < B; ++i) heap.emplace_back(cur(i), i);
+  std::make_heap(heap.begin(), heap.end());
+  int64_t total = streams;
+  while (!heap.empty()) {
+    std::pop_heap(heap.begin(), heap.end());
+    const size_t i = heap.back().second;
+    heap.pop_back();
+    // one more piece for request i: its pieces must stay >= lo keys, and its
+    // streams' extra items must fit the remaining slots
+    if (((int64_t)len[i] + n[i]) / (n[i] + 1) < lo || total + mult[i] > slots) break;
+    ++n[i];
+    total += mult[i];
+    heap.emplace_back(cur(i), i);
+    std::push_heap(heap.begin(), heap.end());
   }
-  return (int)(32 * b);
+  for (size_t i = 0; i < B; ++i) {
+    const int64_t piece = (cur(i) + 31) / 32 * 32;            // equal 32-aligned pieces
+    out[i] = (int)std::min<int64_t>(std::max<int64_t>(piece, 32), kMaxSplit);
+  }
+  return out;
 }
 
 spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
@@ -341,18 +371,26 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
       rows_max = std::max(rows_max, hpg[i] * n);
     }
     const int64_t slots = (int64_t)device_cus() * (bf ? groups_per_cu((rows_max + 15) / 16) : 2);
-    P.split = attn->split_kv > 0 ? attn->split_kv : auto_split(len, mult, rows_max, slots);
+    std::vector<int> plen;
+    if (attn->split_kv > 0) {
+      plen.resize(P.B);
+      for (int i = 0; i < P.B; ++i) plen[i] = piece_len(len[i], attn->split_kv);
+    } else {
+      plen = piece_lengths(len, mult, rows_max, slots);
+    }
+    P.split = 0;
+    for (int i = 0; i < P.B; ++i) P.split = std::max(P.split, plen[i]);
     int64_t part = 0;
     int nr = 1;
     {
       int64_t n_items = 0;
-      for (int i = 0; i < P.B; ++i) n_items += (int64_t)pieces_for(len[i], P.split) * mult[i];
+      for (int i = 0; i < P.B; ++i) n_items += (int64_t)((len[i] + plen[i] - 1) / plen[i]) * mult[i];
       P.items.reserve((size_t)n_items);
     }
     for (int i = 0; i < P.B; ++i) {
       ReqInfo& q = P.reqs[i];
       const int L = len[i];
-      const int piece = piece_len(L, P.split);
+      const int piece = plen[i];
       q.nseg = (L + piece - 1) / piece;
       q.part0 = (int32_t)part;
       if (q.nseg > 1) part += (int64_t)q.nseg * q.nq * Hq;
