@@ -10,17 +10,28 @@
 // l % 16, k = 8 (l / 16) .. +7 of a 16-row block, for the A (hidden) and the
 // B (weight) operand alike, and holds C[4 (l / 16) + i][l % 16].
 //
-// A work-group (4 waves) computes a tile of 16 MB rows x 256 vocabulary
-// entries: wave w owns entries 64 w .. 64 w + 63 (four 16-column blocks) of
-// every row block.  32-k slices of the hidden rows and the weight rows
-// stream HBM -> LDS through an NS-stage ring of direct buffer -> LDS
-// transfers (the attention kernel's ring); the hidden rows are re-read by
-// every vocabulary tile (they stay in L2), each weight byte is read by the
-// work-groups of its vocabulary tile, which are launched together on one
-// XCD so that only the first of them reads it from HBM.
+// A work-group (WR x WC = 4 x 2 waves, two per SIMD) computes a tile of
+// 16 RB WR rows x 256 vocabulary entries; wave (wr, wc) owns row blocks
+// RB wr .. RB wr + RB - 1 and column blocks CB wc .. CB wc + CB - 1 (CB =
+// 16 / WC), so each slice of k is read from LDS (RB + CB) times per wave
+// instead of once per row block and column block.  64-k slices of the hidden
+// rows and the weight rows (one 128-byte cache line per row) stream L2 ->
+// LDS through an NS-stage ring of direct buffer -> LDS transfers (the
+// attention kernel's ring); all of a slice's operands are read into
+// registers before its MFMAs.
+//
+// What bounds it: every CU fetches its operand lines from L2 at a roughly
+// fixed rate (its vector L1 keeps a bounded number of misses in flight), so
+// the time goes with the cache lines a CU fetches per slice, hidden rows +
+// 256 weight rows, and with the rounds of work-groups over the CUs.  Tall
+// tiles fetch fewer lines per flop but fill the LDS with fewer ring stages;
+// lmh_geometry() picks the tile height per shape from that cost, and the row
+// tiles of one vocabulary tile run together on one XCD, so that each weight
+// line comes from HBM once and the hidden rows stay in L2.
 #include "sv_internal.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace sv {
 namespace {
@@ -29,16 +40,33 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-constexpr int kRowB = 64;            // bytes of one 32-k row slice in LDS
-#ifndef SV_LMH_WAVES
-#define SV_LMH_WAVES 8
+#ifndef SV_LMH_KS
+#define SV_LMH_KS 2
 #endif
-#ifndef SV_LMH_MAXROWS
-#define SV_LMH_MAXROWS 128
+#ifndef SV_LMH_HOIST
+#define SV_LMH_HOIST 1
 #endif
-constexpr int kLmhWaves = SV_LMH_WAVES;   // waves per work-group
+constexpr int kKS = SV_LMH_KS;       // 32-k halves per slice
+constexpr int kRowB = 64 * kKS;      // bytes of one row slice in LDS
+static_assert(kKS == 1 || kKS == 2, "32- or 64-k slices");
+#ifndef SV_LMH_WR
+#define SV_LMH_WR 4
+#endif
+#ifndef SV_LMH_WC
+#define SV_LMH_WC 2
+#endif
+#ifndef SV_LMH_MAXRB
+#define SV_LMH_MAXRB 4
+#endif
+#ifndef SV_LMH_MAXNS
+#define SV_LMH_MAXNS 4
+#endif
+constexpr int kWR = SV_LMH_WR;       // waves along the rows
+constexpr int kWC = SV_LMH_WC;       // waves along the vocabulary tile
+constexpr int kLmhWaves = kWR * kWC;
 constexpr int kLmhThreads = 64 * kLmhWaves;
-constexpr int kLmhCB = kLmhNT / (16 * kLmhWaves);   // 16-column blocks per wave
+constexpr int kCB = kLmhNT / (16 * kWC);   // 16-column blocks per wave
+static_assert(kCB * 16 * kWC == kLmhNT, "the waves' column blocks tile the vocabulary tile");
 
 template <int N>
 __device__ __forceinline__ void lmh_wait_vm() {
@@ -47,37 +75,34 @@ __device__ __forceinline__ void lmh_wait_vm() {
 }
 __device__ __forceinline__ void lmh_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// 16-byte chunk c of LDS row r sits at chunk c ^ swz(r): the 16 rows one
-// quarter-wave reads (a 16-row block, one chunk each) fall on 16 distinct
-// 4-bank groups.
-__device__ __forceinline__ int lmh_swz(int r) { return (r >> 2) & 3; }
+// 16-byte chunk c of LDS row r sits at chunk c ^ swz(r): the 8 rows that 8
+// consecutive lanes read (one chunk each) cover all 32 banks (128-byte rows:
+// one row per bank sweep; 64-byte rows: two).
+__device__ __forceinline__ int lmh_swz(int r) { return kKS == 2 ? (r & 7) : ((r >> 1) & 3); }
 
-template <int MB>
+template <int RB>
 struct LmhGeo {
-  static constexpr int RA = 16 * MB;                  // hidden rows per tile
+  static constexpr int RA = 16 * RB * kWR;            // hidden rows per tile
   static constexpr int ROWS = RA + kLmhNT;            // LDS rows per stage
   static constexpr int STAGE = ROWS * kRowB;
-  static constexpr int XF = ROWS / 16;                // 1 KB transfers per stage (16 rows each)
+  static constexpr int XF = ROWS * kRowB / 1024;      // 1 KB transfers per stage
   static constexpr int PER = (XF + kLmhWaves - 1) / kLmhWaves;   // per wave (padded with repeats)
+  // ring depth: as many stages as 144 KB of LDS holds, at most SV_LMH_MAXNS
+  static constexpr int FIT = (144 * 1024) / STAGE;
+  static constexpr int NS = FIT < SV_LMH_MAXNS ? FIT : SV_LMH_MAXNS;
+  static_assert(NS >= 2, "two stages at least");
 };
 
-// Ring depth by row blocks: weight-streaming shapes (few rows) keep more
-// stages in flight; the LDS also holds the epilogue's reductions.
-template <int MB>
-struct LmhStages {
-  // as many stages as 144 KB of LDS holds, at most 6
-  static constexpr int fit = (144 * 1024) / LmhGeo<MB>::STAGE;
-  static constexpr int value = fit < 6 ? fit : 6;
-};
-
-template <int MB, int NS, bool BF16OUT>
-__global__ __launch_bounds__(kLmhThreads) void lmh_gemm(LmhParams p) {
+template <int RB, bool BF16OUT>
+// one work-group per CU (its ring fills the LDS): 8 waves are 2 per SIMD
+__global__ __launch_bounds__(kLmhThreads) __attribute__((amdgpu_waves_per_eu(kLmhWaves / 4, kLmhWaves / 4))) void lmh_gemm(LmhParams p) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  using G = LmhGeo<MB>;
-  constexpr int PER = G::PER;
+  using G = LmhGeo<RB>;
+  constexpr int PER = G::PER, NS = G::NS, CB = kCB;
   __shared__ __attribute__((aligned(1024))) char lds[NS * G::STAGE];
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wr = w / kWC, wc = w % kWC;
   const int l16 = lane & 15, grp = lane >> 4;
 
   // block -> (row tile, vocabulary tile): the row tiles of one vocabulary
@@ -88,23 +113,27 @@ __global__ __launch_bounds__(kLmhThreads) void lmh_gemm(LmhParams p) {
   const int g = blockIdx.x / (8 * T), r8 = blockIdx.x % (8 * T);
   const int mt = r8 / 8, nt = g * 8 + (r8 % 8);
   if (nt >= p.ntiles) return;                       // uniform: past the vocabulary
-  const int m0 = mt * G::RA, n0 = nt * kLmhNT;
-  const int mrows = min(G::RA, p.M - m0), ncols = min(kLmhNT, p.V - n0);
+  const int m0 = mt * p.tile_rows, n0 = nt * kLmhNT;
+  const int mrows = min(p.tile_rows, p.M - m0), ncols = min(kLmhNT, p.V - n0);
   if (mrows <= 0) return;
   // buffer resources over this tile's rows: loads past them read zeros
   const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(p.hidden + (int64_t)m0 * p.h_st), 0, (uint32_t)(mrows * p.h_st * 2), 0x00020000);
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(p.weight + (int64_t)n0 * p.w_st), 0, (uint32_t)(ncols * p.w_st * 2), 0x00020000);
-  // this lane's byte offset in each of its transfers (the k slice's start is soffset)
+  // this lane's byte offset in each of its transfers (the k slice's start is
+  // soffset): transfer j fills 1 KB of LDS rows from row (1024 / kRowB) j on,
+  // lane l the 16 bytes at LDS chunk l % (kRowB / 16) of row (1024 / kRowB) j
+  // + l / (kRowB / 16)
   uint32_t off[PER];
   bool isw[PER];
   int dst[PER];
 #pragma unroll
   for (int q = 0; q < PER; ++q) {
-    const int j = (w + kLmhWaves * q) % G::XF;       // transfer index (repeats pad the last wave)
-    const int row = 16 * j + lane / 4;               // LDS row of this lane's chunk
-    const int chunk = (lane & 3) ^ lmh_swz(row);     // global chunk that lands at LDS chunk lane & 3
+    const int j = (w + kLmhWaves * q) % G::XF;       // transfer index (repeats pad the last waves)
+    constexpr int CPR = kRowB / 16;                  // chunks per row
+    const int row = (1024 / kRowB) * j + lane / CPR; // LDS row of this lane's chunk
+    const int chunk = (lane % CPR) ^ lmh_swz(row);   // global chunk that lands at LDS chunk lane % CPR
     isw[q] = row >= G::RA;
     const int grow = isw[q] ? row - G::RA : row;
     off[q] = (uint32_t)grow * (uint32_t)((isw[q] ? p.w_st : p.h_st) * 2) + (uint32_t)chunk * 16u;
@@ -112,37 +141,33 @@ __global__ __launch_bounds__(kLmhThreads) void lmh_gemm(LmhParams p) {
   }
   auto issue = [&](int stage, int t) {
     char* base = lds + stage * G::STAGE;
-    const uint32_t soff = (uint32_t)t * 64u;          // 32 bf16 of k per slice
+    const uint32_t soff = (uint32_t)t * kRowB;        // 32 kKS bf16 of k per slice
 #pragma unroll
     for (int q = 0; q < PER; ++q)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(isw[q] ? rw : rh, (lds_void_t*)(base + dst[q]), 16, off[q], soff, 0,
                                                0);
   };
 
-  constexpr int CB = kLmhCB;
-  f32x4 acc[MB][CB];
+  f32x4 acc[RB][CB];
 #pragma unroll
-  for (int rb = 0; rb < MB; ++rb)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // LDS read offsets (stage 0) of this lane's A rows and B rows
-  uint32_t aoff[MB], boff[CB];
+  // LDS read offsets in a stage: a 16-row block starts at a multiple of 16,
+  // so swz(row) = swz(l16) and the chunk of k half h is (4 h + grp) ^ swz(l16)
+  uint32_t ch[kKS];
 #pragma unroll
-  for (int rb = 0; rb < MB; ++rb) {
-    const int row = 16 * rb + l16;
-    aoff[rb] = row * kRowB + ((grp ^ lmh_swz(row)) * 16);
-  }
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb) {
-    const int row = G::RA + 16 * CB * w + 16 * cb + l16;
-    boff[cb] = row * kRowB + ((grp ^ lmh_swz(row)) * 16);
-  }
+  for (int h = 0; h < kKS; ++h) ch[h] = (uint32_t)(((4 * h + grp) ^ lmh_swz(l16)) * 16);
+  const uint32_t abase = (uint32_t)(16 * RB * wr + l16) * kRowB;
+  const uint32_t bbase = (uint32_t)(G::RA + 16 * CB * wc + l16) * kRowB;
 
-  const int nk = p.K / 32;
+  const int nk = (p.K + 32 * kKS - 1) / (32 * kKS);
+  const int nfull = p.K / (32 * kKS);               // 64-k slices, K % 64 == 32: the last one holds 32 k only
 #pragma unroll
   for (int st = 0; st < NS - 1; ++st)
     if (st < nk) issue(st, st);
-  for (int t = 0; t < nk; ++t) {
+  auto slice = [&](int t, auto full_c) {
+    constexpr bool FULL = decltype(full_c)::value;
     const int stage = t % NS;
     // this wave's transfers of slice t have landed (later ones may still fly)
     if (t + NS - 2 < nk) lmh_wait_vm<PER * (NS - 2)>();
@@ -150,16 +175,42 @@ __global__ __launch_bounds__(kLmhThreads) void lmh_gemm(LmhParams p) {
     lmh_barrier();                  // everyone's have; stage (t - 1) % NS is free
     if (t + NS - 1 < nk) issue((t + NS - 1) % NS, t + NS - 1);
     const char* sb = lds + stage * G::STAGE;
-    bf16x8 bop[CB];
+    constexpr int NH = FULL ? kKS : 1;
+    bf16x8 a[kKS][RB], b[kKS][CB];
+    auto rd = [&](int h) {
 #pragma unroll
-    for (int cb = 0; cb < CB; ++cb) bop[cb] = *reinterpret_cast<const bf16x8*>(sb + boff[cb]);
+      for (int cb = 0; cb < CB; ++cb) b[h][cb] = *reinterpret_cast<const bf16x8*>(sb + bbase + cb * 16 * kRowB + ch[h]);
 #pragma unroll
-    for (int rb = 0; rb < MB; ++rb) {
-      const bf16x8 aop = *reinterpret_cast<const bf16x8*>(sb + aoff[rb]);
+      for (int rb = 0; rb < RB; ++rb) a[h][rb] = *reinterpret_cast<const bf16x8*>(sb + abase + rb * 16 * kRowB + ch[h]);
+    };
+    auto mm = [&](int h) {
 #pragma unroll
-      for (int cb = 0; cb < CB; ++cb) acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, bop[cb], acc[rb][cb], 0, 0, 0);
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[h][rb], b[h][cb], acc[rb][cb], 0, 0, 0);
+    };
+#if SV_LMH_HOIST
+    // every read of the slice is issued before its first MFMA
+#pragma unroll
+    for (int h = 0; h < NH; ++h) rd(h);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int h = 0; h < NH; ++h) mm(h);
+#else
+    // one 32-k half at a time: its operands into registers, then its MFMAs
+    // (the other wave on the SIMD covers the reads' latency)
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      rd(h);
+      __builtin_amdgcn_sched_barrier(0);
+      mm(h);
+      __builtin_amdgcn_sched_barrier(0);
     }
-  }
+#endif
+  };
+  for (int t = 0; t < nfull; ++t) slice(t, std::true_type{});
+  if (nk > nfull) slice(nfull, std::false_type{});
   lmh_wait_vm<0>();
   __syncthreads();                  // the ring is no longer read: reuse its LDS
 
@@ -167,19 +218,18 @@ __global__ __launch_bounds__(kLmhThreads) void lmh_gemm(LmhParams p) {
   // statistics of each row over the tile's 256 entries are taken on the
   // stored values: the maximum, then the sum of exp(l - max) in fp64, lane
   // sums in column-block order, then across the 16 lanes of a row by an xor
-  // butterfly, then across the four waves in wave order.
-  constexpr int NW = kLmhWaves;
-  float* red_m = reinterpret_cast<float*>(lds);                     // [NW][RA]
-  double* red_s = reinterpret_cast<double*>(lds + NW * G::RA * 4);  // [NW][RA]
-  float val[MB][CB][4];
+  // butterfly, then across the WC waves of the row in wave order.
+  float* red_m = reinterpret_cast<float*>(lds);                      // [WC][RA]
+  double* red_s = reinterpret_cast<double*>(lds + kWC * G::RA * 4);  // [WC][RA]
+  float val[RB][CB][4];
 #pragma unroll
-  for (int rb = 0; rb < MB; ++rb)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
-      const int col = 16 * CB * w + 16 * cb + l16;
+      const int col = 16 * CB * wc + 16 * cb + l16;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = 16 * rb + 4 * grp + i;
+        const int row = 16 * (RB * wr + rb) + 4 * grp + i;
         float v = acc[rb][cb][i];
         if constexpr (BF16OUT) {
           const uint32_t u = __float_as_uint(v);
@@ -194,75 +244,95 @@ __global__ __launch_bounds__(kLmhThreads) void lmh_gemm(LmhParams p) {
       }
     }
 #pragma unroll
-  for (int rb = 0; rb < MB; ++rb)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float m = val[rb][0][i];
 #pragma unroll
       for (int cb = 1; cb < CB; ++cb) m = fmaxf(m, val[rb][cb][i]);
       for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o));
-      if (l16 == 0) red_m[w * G::RA + 16 * rb + 4 * grp + i] = m;
+      if (l16 == 0) red_m[wc * G::RA + 16 * (RB * wr + rb) + 4 * grp + i] = m;
     }
   __syncthreads();
   auto row_max = [&](int row) {
     float m = red_m[row];
 #pragma unroll
-    for (int x = 1; x < NW; ++x) m = fmaxf(m, red_m[x * G::RA + row]);
+    for (int x = 1; x < kWC; ++x) m = fmaxf(m, red_m[x * G::RA + row]);
     return m;
   };
 #pragma unroll
-  for (int rb = 0; rb < MB; ++rb)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = 16 * rb + 4 * grp + i;
+      const int row = 16 * (RB * wr + rb) + 4 * grp + i;
       const float m = row_max(row);
       double sm = 0.0;
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb) sm += (double)exp_rel(val[rb][cb][i], m);
       for (int o = 1; o < 16; o <<= 1) sm += __shfl_xor(sm, o);
-      if (l16 == 0) red_s[w * G::RA + row] = sm;
+      if (l16 == 0) red_s[wc * G::RA + row] = sm;
     }
   __syncthreads();
   for (int row = threadIdx.x; row < mrows; row += kLmhThreads) {
     double sm = red_s[row];
 #pragma unroll
-    for (int x = 1; x < NW; ++x) sm += red_s[x * G::RA + row];
+    for (int x = 1; x < kWC; ++x) sm += red_s[x * G::RA + row];
     p.tiles[(int64_t)(m0 + row) * p.ntiles + nt] = ChunkStat{sm, row_max(row), 0.f};
   }
 #endif
 }
 
-template <int MB>
-hipError_t launch_mb(const LmhParams& p, hipStream_t s) {
+template <int RB>
+hipError_t launch_rb(const LmhParams& p, hipStream_t s) {
   const int groups = (p.ntiles + 7) / 8;
   const dim3 grid((unsigned)(groups * 8 * p.m_tiles));
-  constexpr int NS = LmhStages<MB>::value;
-  if (p.out_bf16) lmh_gemm<MB, NS, true><<<grid, dim3(kLmhThreads), 0, s>>>(p);
-  else lmh_gemm<MB, NS, false><<<grid, dim3(kLmhThreads), 0, s>>>(p);
+  if (p.out_bf16) lmh_gemm<RB, true><<<grid, dim3(kLmhThreads), 0, s>>>(p);
+  else lmh_gemm<RB, false><<<grid, dim3(kLmhThreads), 0, s>>>(p);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int lmh_row_blocks(int M) {
-  const int tiles = (M + SV_LMH_MAXROWS - 1) / SV_LMH_MAXROWS;
-  const int rows = (M + tiles - 1) / tiles;
-  return (rows + 15) / 16;
+// Tile height for M rows and ntiles vocabulary tiles.  Every CU fetches
+// its operands from L2 at a fixed rate of cache lines, so a launch costs
+// about (rounds of work-groups over the CUs) x (lines per k slice: the
+// tile's hidden rows + 256 weight rows); the height with the lowest cost
+// wins (ties: the lower one, fewer idle MFMAs), and its row tiles are
+// balanced (rows past M read as zeros and cost no line).
+LmhGeometry lmh_geometry(int M, int ntiles, int cus) {
+  LmhGeometry best{};
+  int64_t best_cost = -1;
+  for (int rb = 1; rb <= SV_LMH_MAXRB; ++rb) {
+    const int ra = 16 * kWR * rb;
+    const int m_tiles = (M + ra - 1) / ra;
+    const int rows = (M + m_tiles - 1) / m_tiles;
+    const int64_t groups = (int64_t)m_tiles * ntiles;
+    const int64_t cost = ((groups + cus - 1) / cus) * (int64_t)(rows + kLmhNT);
+    if (best_cost < 0 || cost < best_cost) {
+      best_cost = cost;
+      best = LmhGeometry{rb, rows, m_tiles};
+    }
+  }
+  return best;
 }
 
 hipError_t launch_lmh(const LmhParams& p, hipStream_t s) {
-  switch (lmh_row_blocks(p.M)) {
-    case 1: return launch_mb<1>(p, s);
-    case 2: return launch_mb<2>(p, s);
-    case 3: return launch_mb<3>(p, s);
-    case 4: return launch_mb<4>(p, s);
-    case 5: return launch_mb<5>(p, s);
-    case 6: return launch_mb<6>(p, s);
-    case 7: return launch_mb<7>(p, s);
-    case 8: return launch_mb<8>(p, s);
-#if SV_LMH_MAXROWS > 128
-    case 9: return launch_mb<9>(p, s);
-    case 10: return launch_mb<10>(p, s);
+  if (p.M < 1 || p.tile_rows < 1 || p.tile_rows > 16 * kWR * p.rb || p.m_tiles != (p.M + p.tile_rows - 1) / p.tile_rows)
+    return hipErrorInvalidValue;
+  switch (p.rb) {
+    case 1: return launch_rb<1>(p, s);
+    case 2: return launch_rb<2>(p, s);
+#if SV_LMH_MAXRB >= 3
+    case 3: return launch_rb<3>(p, s);
+#endif
+#if SV_LMH_MAXRB >= 4
+    case 4: return launch_rb<4>(p, s);
+#endif
+#if SV_LMH_MAXRB >= 8
+    case 5: return launch_rb<5>(p, s);
+    case 6: return launch_rb<6>(p, s);
+    case 7: return launch_rb<7>(p, s);
+    case 8: return launch_rb<8>(p, s);
 #endif
     default: return hipErrorInvalidValue;
   }

@@ -537,7 +537,8 @@ spec_status_t check_lm(const spec_lm_head_args_t* lm) {
       lm->weight_stride % 8)
     return SPEC_ERR_INVALID_ARG;
   // each work-group's rows are addressed with 32-bit offsets
-  if ((int64_t)sv::kLmhNT * lm->weight_stride * 2 >= INT32_MAX || (int64_t)128 * lm->hidden_stride * 2 >= INT32_MAX)
+  if ((int64_t)sv::kLmhNT * lm->weight_stride * 2 >= INT32_MAX ||
+      (int64_t)sv::kLmhMaxTileRows * lm->hidden_stride * 2 >= INT32_MAX)
     return SPEC_ERR_UNSUPPORTED;
   return SPEC_OK;
 }
@@ -684,7 +685,10 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     g.K = lm->hidden_dim;
     g.V = acc->vocab;
     g.ntiles = (acc->vocab + sv::kLmhNT - 1) / sv::kLmhNT;
-    g.m_tiles = (g.M + 16 * sv::lmh_row_blocks(g.M) - 1) / (16 * sv::lmh_row_blocks(g.M));
+    const sv::LmhGeometry geo = sv::lmh_geometry(g.M, g.ntiles, device_cus());
+    g.rb = geo.rb;
+    g.tile_rows = geo.tile_rows;
+    g.m_tiles = geo.m_tiles;
     g.out_bf16 = acc->dtype == SPEC_BF16;
     if (lm->event_begin && hipEventRecord(static_cast<hipEvent_t>(lm->event_begin), s) != hipSuccess) return SPEC_ERR_HIP;
     if (sv::launch_lmh(g, s) != hipSuccess) return SPEC_ERR_HIP;

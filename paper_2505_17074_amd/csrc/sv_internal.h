@@ -169,12 +169,18 @@ struct LmhParams {
   int64_t o_st;
   ChunkStat* tiles;         // [M, ntiles] per-tile (sum of exp(l - max), max)
   int32_t M, K, V, ntiles;
-  int32_t m_tiles;          // row tiles of 16 * MB rows
+  int32_t m_tiles;          // row tiles of tile_rows rows (the last one may be shorter)
+  int32_t tile_rows;        // <= the kernel's tile height 64 rb
+  int32_t rb;               // 16-row blocks per wave: tile height 64 rb
   int32_t out_bf16;
 };
-// Rows per row tile (in units of 16) for M rows: the fewest tiles of at most
-// 128 rows, each as small as the split allows.
-int lmh_row_blocks(int M);
+struct LmhGeometry {
+  int32_t rb, tile_rows, m_tiles;
+};
+constexpr int kLmhMaxTileRows = 256;   // 16 x waves along the rows x row blocks per wave, at most
+// The tile height and row tiles for M rows, ntiles vocabulary tiles and cus
+// compute units.
+LmhGeometry lmh_geometry(int M, int ntiles, int cus);
 hipError_t launch_lmh(const LmhParams& p, hipStream_t s);
 // Chunk statistics [Nq, nch] (the decision kernel's input) folded from the
 // LM head's tile statistics, plus the row-statistics kernel's other duties

@@ -70,6 +70,10 @@ CASES = [
     ("ragged_gqa_b128", 24, 256, 5000),  # 2 row tiles
     ("tree15_b64", 3, 512, 3000),        # token tree, every row's statistics from the GEMM
     ("mha7b_b32", 32, 4096, None),       # LLaMA-7B LM head at the full workload (160 rows)
+    ("ragged_gqa_b128", 128, 4096, None),  # full workload: 716 rows, 192-row tiles
+    ("tree15_b64", 64, 4096, None),      # full workload: 960 rows, 256-row tiles
+    ("tiny_f32", 5, 96, 700),            # hidden width 96: a 64-k slice, then a 32-k tail slice
+    ("mha7b_b32", 2, 32, 513),           # hidden width 32: the tail slice alone
 ]
 
 
