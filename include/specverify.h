@@ -52,6 +52,17 @@
  *     check is then the only work enqueued, and no output is touched).  Without the check an out-of-range token id is
  *     clamped into [0, V): its results are meaningless, but nothing outside
  *     the arguments is read.
+ *   - The device workspace needs no initialisation and may hold anything
+ *     between calls: every byte a call reads is written earlier in the same
+ *     call, except the split-KV arrival counters, which carry a tag that is
+ *     new on every call and start over when it does not match.
+ *   - When the verify attention cuts a request's KV range into pieces, the
+ *     last piece of each (request, KV head, head group) to finish combines
+ *     the pieces' partial outputs (bf16 inputs, partial blocks up to 64 KB
+ *     per stream); otherwise a separate combine kernel follows.  The
+ *     environment variable SPEC_FUSED_COMBINE_MAX_BYTES (a byte count)
+ *     replaces the 64 KB limit; the outputs agree either way within the
+ *     attention tolerance, and each choice is deterministic.
  *   - Results are deterministic: the same inputs give bit-identical outputs
  *     (fixed reduction orders, no floating-point atomics).
  */

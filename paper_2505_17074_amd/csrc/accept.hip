@@ -44,6 +44,21 @@
 namespace sv {
 namespace {
 
+// Diagnostic builds only (-DSV_ACC_TRACE): per work-group phase timestamps
+// of the acceptance kernels on the device's constant-rate clock, read back
+// by sv_acc_trace_copy, for measuring where a kernel's time goes.
+#ifdef SV_ACC_TRACE
+constexpr int kTraceBlocks = 16384, kTracePhases = 8;
+__device__ unsigned long long g_acc_trace[2][kTraceBlocks][kTracePhases];
+#define SV_TRACE(kern, k)                                                         \
+  do {                                                                            \
+    if (threadIdx.x == 0 && blockIdx.x < kTraceBlocks)                            \
+      g_acc_trace[kern][blockIdx.x][k] = wall_clock64();                          \
+  } while (0)
+#else
+#define SV_TRACE(kern, k) ((void)0)
+#endif
+
 __device__ __forceinline__ float ld(const float* p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float ld(const uint16_t* p, int64_t i) {
   return __uint_as_float(static_cast<uint32_t>(p[i]) << 16);
@@ -160,6 +175,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
     row = (ni > 0 && su < p.B * ni) ? (su / ni) * p.topo.nodes + p.topo.inner[su % ni] : -1;
   }
   const T* lp = static_cast<const T*>(p.logits) + (int64_t)max(row, 0) * p.l_st;
+  SV_TRACE(0, 0);
   // the first B work-groups (the grid has at least B of them) bring request
   // blockIdx.x's entry of the staged table into device memory and clear its
   // ticket, for the decision kernel that follows on the stream
@@ -200,6 +216,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
 #pragma unroll
     for (int sc = 0; sc < SUB; ++sc) redf[sc][wv] = m[sc];
   __syncthreads();
+  SV_TRACE(0, 1);
   double sm[SUB];
 #pragma unroll
   for (int sc = 0; sc < SUB; ++sc) {
@@ -218,6 +235,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_rowstats(AccParams p) {
     const double tot = (redd[sc][0] + redd[sc][1]) + (redd[sc][2] + redd[sc][3]);
     if (c0 + sc < p.nch) p.rowstats[(int64_t)row * p.nch + c0 + sc] = ChunkStat{tot, m[sc], 0.f};
   }
+  SV_TRACE(0, 2);
 }
 
 __device__ __forceinline__ int node_parent(const AccParams& p, int n) {
@@ -307,6 +325,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   __shared__ int s_par[kMaxNodes], s_dep[kMaxNodes], s_qr[kMaxNodes];
   const int i = blockIdx.x / p.nch, c = blockIdx.x % p.nch;
   const int tid = threadIdx.x, wv = tid >> 6, ln = tid & 63;
+  SV_TRACE(1, 0);
   const ReqInfo rq = p.reqs[i];
   const int N = rq.nq;
   const T* L = static_cast<const T*>(p.logits);
@@ -350,6 +369,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
     }
   }
   __syncthreads();
+  SV_TRACE(1, 1);
 
   if (tid < 64) {
     // one lane per non-root node: the test of Eq. (1) against its parent's rows
@@ -382,6 +402,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
     }
   }
   __syncthreads();
+  SV_TRACE(1, 2);
   const Decision d = s_dec;
   const double invZ = 1.0 / d.Z;
   bool residual = d.qrow >= 0;
@@ -414,6 +435,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
       for (int k = 0; k < 16; ++k) sm += (double)exp_rel(x[k], m);
       sm = block_sum(sm, redd);
     }
+    SV_TRACE(1, 3);
     if (tid == 0) {
       if (residual) {
         if (p.nch == 1) s_mass[0] = sm;
@@ -430,6 +452,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
         const int t = __hip_atomic_fetch_add(p.tickets + i, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         s_last = (t == p.nch - 1);
       }
+      SV_TRACE(1, 4);
     }
   }
   __syncthreads();
@@ -472,6 +495,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
     }
     __syncthreads();
   }
+  SV_TRACE(1, 5);
   const float u = p.uniforms[rq.q0 + N - 1];
   if (tid == 0) {
     const double tot = s_tot;
@@ -504,6 +528,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
     }
   }
   __syncthreads();
+  SV_TRACE(1, 6);
   const int cc = s_chunk;
   const float mcc = s_mcc;
   float x[16], q[16];
@@ -566,6 +591,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
     p.acc_len[i] = d.len;
     if (p.acc_node) p.acc_node[i] = d.node;
   }
+  SV_TRACE(1, 7);
 }
 
 // Sequential sibling verification over a token tree (SpecInfer's multi-step
@@ -859,6 +885,12 @@ hipError_t launch_foldstats(const AccParams& p, const ChunkStat* tiles, int ntil
   acc_foldstats<<<grid, dim3(kAccThreads), 0, s>>>(p, tiles, ntiles);
   return hipGetLastError();
 }
+
+#ifdef SV_ACC_TRACE
+extern "C" __attribute__((visibility("default"))) int sv_acc_trace_copy(void* dst, size_t bytes) {
+  return (int)hipMemcpyFromSymbol(dst, HIP_SYMBOL(g_acc_trace), bytes);
+}
+#endif
 
 hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_t s) {
   if (p.bf16) acc_validate<uint16_t><<<1, kAccThreads, 0, s>>>(p, flag);

@@ -355,6 +355,106 @@ struct WavesPerEu {
   static constexpr int value = W == 5 ? SV_WPE_W5 : (W >= 3 ? SV_WPE_W34 : 1);
 };
 
+// Agent-scope (all XCDs) stores of two floats for the fused combine's
+// hand-over (the combine reads them with agent-scope loads).  On gfx950 such a store is written through to the
+// device coherence point and completes (vmcnt) only once it is there; such a
+// load reads from that point, never a stale line of this XCD's L2.  A piece
+// checks in only after its stores have completed, and the last piece loads
+// the partials only after its check-in returned, so it reads every piece's.
+// (Release/acquire fences would write back and invalidate the whole L2 of
+// the XCD at every piece's end: measured 80% slower on long-context GQA.)
+__device__ __forceinline__ void st_dev2(float* p, float a, float b) {
+  const unsigned long long v = (unsigned long long)__float_as_uint(a) | ((unsigned long long)__float_as_uint(b) << 32);
+  __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Arrival of one piece of a split stream on the stream's counter
+// ((call tag << 32) | arrivals so far): a counter holding another tag starts
+// over.  Returns whether this piece is the stream's last (the total-th).
+// Every failed exchange means another piece's succeeded in between, so the
+// loop ends after at most `total` tries; the bound only guards that.
+__device__ __forceinline__ bool arrive_last(unsigned long long* ctr, uint32_t tag, int total) {
+  unsigned long long old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  unsigned long long nw = 0;
+  for (int tries = 0; tries <= total + 1; ++tries) {
+    nw = ((uint32_t)(old >> 32) == tag) ? old + 1 : (((unsigned long long)tag << 32) | 1ull);
+    if (__hip_atomic_compare_exchange_strong(ctr, &old, nw, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT))
+      return (uint32_t)nw == (uint32_t)total;
+  }
+  return false;
+}
+
+// The split combine of one stream (rows = heads x verify positions of one
+// request, KV head and head group), by the work-group of its last piece:
+//   O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,  M = max_s m_s,
+// the pieces summed in index order.  Every (row, piece) pair's (m, l) comes
+// into LDS at once; the rows' weights replace the maxima there, beside the
+// rows' 1 / L.  Then each thread takes 16-byte column groups of two rows at
+// a time, eight pieces' loads in flight.  The partials are read with
+// agent-scope buffer loads (sc1) from the request's block of partial rows.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+constexpr int kCpolAgent = 16;        // the sc1 bit of a buffer instruction's cache policy
+template <int D>
+__device__ __forceinline__ void combine_stream(const AttnParams& p, const AttnItem& it, char* lds) {
+  const int n = it.nq, R = it.nheads * n, nseg = it.nseg;
+  const int nth = (int)blockDim.x, tid = (int)threadIdx.x;
+  const int blk_rows = nseg * n * p.Hq;   // the request's partial rows (the host keeps the bytes < 2^31)
+  const __amdgpu_buffer_rsrc_t ro =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(p.part_o + (int64_t)it.part0 * D), 0, blk_rows * D * 4, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rm =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(p.part_ml + it.part0), 0, blk_rows * 8, 0x00020000);
+  auto lrow = [&](int r, int sg) -> int {
+    const int hh = r / n, j = r - hh * n;
+    return (sg * n + j) * p.Hq + it.head_lo + hh;
+  };
+  float2* mlw = reinterpret_cast<float2*>(lds);     // [R][nseg]: (m, l), then (weight, l)
+  float* invl = reinterpret_cast<float*>(mlw + R * nseg);
+  for (int x = tid; x < R * nseg; x += nth) {
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rm, lrow(x / nseg, x % nseg) * 8, 0, kCpolAgent);
+    mlw[x] = make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
+  }
+  __syncthreads();
+  for (int r = tid; r < R; r += nth) {
+    float2* row = mlw + r * nseg;
+    float M = -INFINITY;
+    for (int sg = 0; sg < nseg; ++sg) M = fmaxf(M, row[sg].x);
+    float L = 0.f;
+    for (int sg = 0; sg < nseg; ++sg) {
+      const float w = (row[sg].x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(row[sg].x - M);
+      row[sg].x = w;
+      L += row[sg].y * w;
+    }
+    invl[r] = 1.f / L;
+  }
+  __syncthreads();
+  constexpr int Q = D / 4;                      // 16-byte column groups per row
+  const int units = R * Q;
+  for (int u0 = tid; u0 < units; u0 += 2 * nth) {
+    const int u1 = min(u0 + nth, units - 1);    // a repeat of a valid unit when past the end
+    const int r0 = u0 / Q, c0 = (u0 % Q) * 4, r1 = u1 / Q, c1 = (u1 % Q) * 4;
+    float4 a0 = make_float4(0.f, 0.f, 0.f, 0.f), a1 = a0;
+#pragma unroll 8
+    for (int sg = 0; sg < nseg; ++sg) {
+      const u32x4 v0 = __builtin_amdgcn_raw_buffer_load_b128(ro, (lrow(r0, sg) * D + c0) * 4, 0, kCpolAgent);
+      const u32x4 v1 = __builtin_amdgcn_raw_buffer_load_b128(ro, (lrow(r1, sg) * D + c1) * 4, 0, kCpolAgent);
+      const float w0 = mlw[r0 * nseg + sg].x, w1 = mlw[r1 * nseg + sg].x;
+      a0.x += w0 * __uint_as_float(v0.x); a0.y += w0 * __uint_as_float(v0.y);
+      a0.z += w0 * __uint_as_float(v0.z); a0.w += w0 * __uint_as_float(v0.w);
+      a1.x += w1 * __uint_as_float(v1.x); a1.y += w1 * __uint_as_float(v1.y);
+      a1.z += w1 * __uint_as_float(v1.z); a1.w += w1 * __uint_as_float(v1.w);
+    }
+    auto store = [&](int r, int c, float4 a) {
+      const int hh = r / n, j = r - hh * n;
+      const float sc = invl[r];
+      *reinterpret_cast<float4*>(p.out + ((int64_t)(it.q0 + j) * p.Hq + it.head_lo + hh) * D + c) =
+          make_float4(a.x * sc, a.y * sc, a.z * sc, a.w * sc);
+    };
+    store(r0, c0, a0);
+    if (u0 + nth < units) store(r1, c1, a1);
+  }
+}
+
 // PG: paged KV cache.  A tile (32 keys, 32-aligned) never straddles a page
 // (pages hold a multiple of 32 tokens), so each tile's transfers take a buffer
 // resource based at its page, built from the block table entry (a
@@ -541,7 +641,14 @@ void attn_split_mfma(AttnParams p) {
     return (r < R && o >= 0 && o < lim) ? o : -1;
   };
   const int64_t o0 = out_row(w * 16 + c16);
-  if (it.seg >= 0 && grp == 0 && o0 >= 0) p.part_ml[o0] = make_float2(S.m, l);
+  // The fused combine's partials are written through to the device coherence
+  // point (agent-scope stores) for the stream's last piece, which may run on
+  // another XCD, to read back the same way.
+  const bool publish = it.seg >= 0 && p.fused;
+  if (it.seg >= 0 && grp == 0 && o0 >= 0) {
+    if (publish) st_dev2(reinterpret_cast<float*>(p.part_ml + o0), S.m, l);
+    else p.part_ml[o0] = make_float2(S.m, l);
+  }
   __syncthreads();
   // whole-row writes: D/4 lanes per row, 64*4/D rows per pass
   constexpr int LPR = D / 4, RPP = 64 / LPR;
@@ -552,7 +659,24 @@ void attn_split_mfma(AttnParams p) {
     const int64_t o = out_row(w * 16 + rl);
     if (o < 0) continue;
     const float4 v = *reinterpret_cast<const float4*>(ost + rl * (D + 4) + e4);
-    *reinterpret_cast<float4*>((it.seg < 0 ? p.out : p.part_o) + o * D + e4) = v;
+    float* dst = (it.seg < 0 ? p.out : p.part_o) + o * D + e4;
+    if (publish) {
+      st_dev2(dst, v.x, v.y);
+      st_dev2(dst + 2, v.z, v.w);
+    } else {
+      *reinterpret_cast<float4*>(dst) = v;
+    }
+  }
+  if (publish) {
+    // Check in on the stream's counter once this work-group's partial stores
+    // have completed; the stream's last piece combines.
+    __shared__ int s_last;
+    wait_vm<0>();
+    __syncthreads();
+    if (threadIdx.x == 0) s_last = arrive_last(p.counters + it.stream, p.call_tag, it.nseg) ? 1 : 0;
+    __syncthreads();
+    if (!s_last) return;
+    combine_stream<D>(p, it, lds);
   }
 #endif
 }
@@ -750,6 +874,21 @@ hipError_t launch_mfma(const AttnParams& p, int nr, hipStream_t s) {
 }  // namespace
 
 int max_rows_per_item(int dtype_bf16, int D) { return dtype_bf16 ? 80 : 4096 / D; }
+
+int attn_lds_bytes(int D, int nr) {
+  auto bytes = [&](auto d) -> int {
+    constexpr int DD = decltype(d)::value;
+    switch (nr) {
+      case 1: return AttnLds<DD, 1, SV_NS_W1>::BYTES;
+      case 2: return AttnLds<DD, 2, SV_NS_W2>::BYTES;
+      case 3: return AttnLds<DD, 3, SV_NS_W3>::BYTES;
+      case 4: return AttnLds<DD, 4, SV_NS_W4>::BYTES;
+      case 5: return AttnLds<DD, 5, SV_NS_W5>::BYTES;
+      default: return 0;
+    }
+  };
+  return D == 64 ? bytes(std::integral_constant<int, 64>{}) : bytes(std::integral_constant<int, 128>{});
+}
 
 hipError_t launch_attention(const AttnParams& p, int dtype_bf16, int nr_max, hipStream_t s) {
   hipError_t e = hipSuccess;

@@ -4,7 +4,11 @@
 
 #include <hip/hip_runtime.h>
 
+#include <unistd.h>
+
 #include <algorithm>
+#include <atomic>
+#include <chrono>
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -39,13 +43,15 @@ struct Plan {
   int64_t parts = 0;      // partial rows
   int nr_max = 1;
   int split = 0;
+  int64_t split_streams = 0;   // (request, KV head, head group) streams cut into pieces
+  bool fused = false;          // the split kernel combines its own partials
   // acceptance
   bool has_acc = false;
   int nch = 0;
   // layout (bytes)
   size_t off_reqs = 0, off_rowreq = 0, off_items = 0, off_nodes = 0, plan_bytes = 0;
   size_t off_acc_reqs = 0, off_acc_nodes = 0, off_tickets = 0;
-  size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_masses = 0, off_flag = 0;
+  size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_masses = 0, off_flag = 0, off_counters = 0;
   size_t device_bytes = 0;
 };
 
@@ -196,6 +202,23 @@ int piece_len(int L, int64_t s) {
 #define SV_MAX_PIECE 4096
 #endif
 constexpr int64_t kMaxPiece = SV_MAX_PIECE;
+// Largest partial block (rows x pieces x d x 4 bytes) of one split stream
+// that the split kernel's last piece combines itself; above it the separate
+// combine kernel spreads the work over the device.  The last piece reads the
+// block alone, after every other piece of the stream has finished: on the
+// ragged GQA batch (streams of <= 55 KB) fusing shortens the attention by
+// 5 us and the step by 10 us, while on the long-context batch (295 KB per
+// stream) it lengthens the attention by 7 us.  The environment variable
+// SPEC_FUSED_COMBINE_MAX_BYTES overrides the limit (tests use it to reach
+// the fused path with any stream).
+constexpr int64_t kFuseMaxBytes = 64 << 10;
+int64_t fuse_max_bytes() {
+  const char* e = std::getenv("SPEC_FUSED_COMBINE_MAX_BYTES");
+  if (!e || !*e) return kFuseMaxBytes;
+  char* end = nullptr;
+  const long long v = std::strtoll(e, &end, 10);
+  return (end && *end == 0 && v >= 0) ? (int64_t)v : kFuseMaxBytes;
+}
 constexpr int64_t kMaxSplit = 1 << 20;
 // Keys per piece of each request's streams (every KV head and head group of
 // a request has the same length).  `slots` = work-groups the device runs at
@@ -394,6 +417,8 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
       q.nseg = (L + piece - 1) / piece;
       q.part0 = (int32_t)part;
       if (q.nseg > 1) part += (int64_t)q.nseg * q.nq * Hq;
+      const int64_t stream0 = P.split_streams;
+      if (q.nseg > 1) P.split_streams += (int64_t)Hkv * groups[i];
       for (int s = 0; s < q.nseg; ++s) {
         for (int g = 0; g < Hkv; ++g) {
           for (int gr = 0; gr < groups[i]; ++gr) {
@@ -411,7 +436,9 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
             it.kv0 = q.kv0;
             it.part0 = q.part0;
             it.node0 = q.node0;
-            it.pad[0] = it.pad[1] = it.pad[2] = 0;
+            it.stream = q.nseg > 1 ? (int32_t)(stream0 + (int64_t)g * groups[i] + gr) : -1;
+            it.nseg = q.nseg;
+            it.pad = 0;
             P.items.push_back(it);
             nr = std::max(nr, (it.nheads * q.nq + 15) / 16);
           }
@@ -435,6 +462,21 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
     if (part >= INT32_MAX) return SPEC_ERR_INVALID_ARG;
     P.parts = part;
     P.nr_max = nr;
+    // The bf16 kernel combines a split stream's partials itself (the last
+    // piece to finish) when the stream's combine weights fit its LDS: rows x
+    // (pieces + 1) floats.  Otherwise the split combine kernel runs after it.
+    if (bf && part > 0) {
+      int64_t lds = 0, blk = 0, stream_bytes = 0;
+      for (int i = 0; i < P.B; ++i) {
+        const ReqInfo& q = P.reqs[i];
+        if (q.nseg <= 1) continue;
+        const int64_t rows = (int64_t)hpg[i] * q.nq;
+        lds = std::max<int64_t>(lds, rows * (2 * (int64_t)q.nseg + 1) * 4);
+        blk = std::max<int64_t>(blk, (int64_t)q.nseg * q.nq * Hq * D * 4);
+        stream_bytes = std::max<int64_t>(stream_bytes, rows * q.nseg * D * 4);
+      }
+      P.fused = lds <= sv::attn_lds_bytes(D, nr) && blk < ((int64_t)1 << 31) && stream_bytes <= fuse_max_bytes();
+    }
   }
 
   // Staged block (the caller's pinned staging buffer; the kernels read it in
@@ -463,6 +505,8 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   off = align_up(off + sizeof(float) * (size_t)P.parts * D);
   P.off_part_ml = off;
   off = align_up(off + sizeof(float) * 2 * (size_t)P.parts);
+  P.off_counters = off;                // the fused combine's arrival counters
+  off = align_up(off + sizeof(unsigned long long) * (size_t)(P.fused ? P.split_streams : 0));
   P.off_rowstats = off;
   off = align_up(off + sizeof(sv::ChunkStat) * (size_t)(P.has_acc ? P.Nq * P.nch : 0));
   P.off_masses = off;
@@ -505,6 +549,20 @@ SideStream* side_stream() {
     S.ready = true;
   }
   return &S;
+}
+
+// A fresh 32-bit tag per call for the fused combine's arrival counters, never
+// 0 (fresh device memory is often zero).  The process's first tag is drawn
+// from the clock and the process id, so memory left by an earlier process
+// is as unlikely to match as anything else.
+uint32_t next_call_tag() {
+  static std::atomic<uint32_t> tag{
+      (uint32_t)std::chrono::steady_clock::now().time_since_epoch().count() * 2654435761u ^ (uint32_t)getpid()};
+  uint32_t t;
+  do {
+    t = tag.fetch_add(1, std::memory_order_relaxed);
+  } while (t == 0);
+  return t;
 }
 
 void write_staging(const Plan& P, void* host) {
@@ -601,7 +659,11 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     a.items = reinterpret_cast<const AttnItem*>(pl + P.off_items);
     a.reqs = reinterpret_cast<const ReqInfo*>(d + P.off_reqs);
     a.row_req = reinterpret_cast<const int32_t*>(d + P.off_rowreq);
-    if (P.parts > 0 && pl != d) {      // the combine runs: mirror its table and map
+    if (P.fused) {
+      a.counters = reinterpret_cast<unsigned long long*>(d + P.off_counters);
+      a.call_tag = next_call_tag();
+      a.fused = 1;
+    } else if (P.parts > 0 && pl != d) {      // the combine kernel runs: mirror its table and map
       const bool mfma = attn->dtype == SPEC_BF16;
       const int64_t threads = mfma ? 64 * (int64_t)P.nr_max : 256;
       const int64_t n16 = (int64_t)(P.off_items / 16);
@@ -711,7 +773,7 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     if (attn->event_begin && hipEventRecord(static_cast<hipEvent_t>(attn->event_begin), st) != hipSuccess)
       return false;
     if (sv::launch_attention(a, attn->dtype == SPEC_BF16, P.nr_max, st) != hipSuccess) return false;
-    if (P.parts > 0 && sv::launch_combine(a, st) != hipSuccess) return false;
+    if (P.parts > 0 && !P.fused && sv::launch_combine(a, st) != hipSuccess) return false;
     if (attn->event_end && hipEventRecord(static_cast<hipEvent_t>(attn->event_end), st) != hipSuccess) return false;
     return true;
   };

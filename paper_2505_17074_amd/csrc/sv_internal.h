@@ -51,7 +51,9 @@ struct AttnItem {
   int32_t kv0;
   int32_t part0;
   int32_t node0;    // the request's first node-table entry (per-request trees)
-  int32_t pad[3];
+  int32_t stream;   // split items: the (request, KV head, head group) stream's arrival counter
+  int32_t nseg;     // the request's KV pieces
+  int32_t pad;
 };
 
 static_assert(sizeof(ReqInfo) == 32, "ReqInfo is copied as two 16-byte units");
@@ -107,6 +109,14 @@ struct AttnParams {
   // entries, read where the host staged them
   const NodeInfo* nodes;
   int32_t per_req;
+  // Split combine inside the split kernel (bf16 path): each split stream's
+  // pieces check in on counters[stream] ((call tag << 32) | arrivals), and
+  // the last one to arrive combines the stream's partials.  The tag is new
+  // on every call, so a counter holding another call's value (or anything
+  // else) starts over at its first arrival and never needs clearing.
+  unsigned long long* counters;
+  uint32_t call_tag;
+  int32_t fused;
 };
 
 // Acceptance scratch: per (row, vocabulary chunk) max and fp64 sum of exp.
@@ -202,6 +212,9 @@ __device__ __forceinline__ float exp_rel(float x, float m) {
 int max_rows_per_item(int dtype_bf16, int D);
 
 hipError_t launch_attention(const AttnParams& p, int dtype_bf16, int nr_max, hipStream_t s);
+// LDS bytes of the bf16 split kernel's build for head dim D and nr row tiles
+// (the fused combine stages its weights there).
+int attn_lds_bytes(int D, int nr);
 hipError_t launch_combine(const AttnParams& p, hipStream_t s);
 // Both acceptance kernels; `mid` (optional) is recorded between them.
 hipError_t launch_accept(const AccParams& p, hipStream_t s, hipEvent_t mid = nullptr);

@@ -323,3 +323,20 @@ def test_per_request_trees_size_like_the_shared_tree(lib):
     per = _ws(_req_trees(ctx, [tree] * 3), _attn(), _acc())
     assert shared[0] == per[0] == B.SPEC_OK
     assert per[2] >= shared[2] + 8 * 21 and per[1] >= shared[1] + 8 * 21
+
+
+def test_fused_combine_counters_in_the_workspace(lib, monkeypatch):
+    """Split streams whose partial blocks are under the planner's limit are
+    combined inside the bf16 split kernel, which needs one arrival counter per
+    split stream in the workspace; the environment limit turns that off, and
+    fp32 inputs (the VALU kernel) never use it."""
+    req = _req(ctx=(3000, 5000))
+    fused = _ws(req, _attn(split_kv=1024), None)           # 16 rows x 5 pieces x 512 B = 40 KB
+    monkeypatch.setenv("SPEC_FUSED_COMBINE_MAX_BYTES", "0")
+    separate = _ws(req, _attn(split_kv=1024), None)
+    monkeypatch.setenv("SPEC_FUSED_COMBINE_MAX_BYTES", "not a number")   # ignored: the default limit
+    assert _ws(req, _attn(split_kv=1024), None) == fused
+    assert fused[0] == separate[0] == B.SPEC_OK and fused[1] == separate[1] + 256
+    monkeypatch.delenv("SPEC_FUSED_COMBINE_MAX_BYTES")
+    f32 = dict(dtype=B.SPEC_F32)
+    assert _ws(req, _attn(split_kv=1024, **f32), None)[1] == separate[1]
