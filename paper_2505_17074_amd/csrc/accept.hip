@@ -278,10 +278,21 @@ __device__ __forceinline__ double final_weight(float l, float q, float M, double
 }
 
 // Device-scope (all XCDs) publication of the chunk masses between the
-// work-groups of one request: the stores write through to the device
-// coherence point, the loads read from it, and the ticket is a device-scope
-// atomic issued after this wave's stores have completed.  No cache-wide
-// write-back is needed since nothing else is handed over.
+// work-groups of one request.  The hand-over rests on how gfx950 executes
+// agent-scope accesses rather than on a release/acquire pair:
+//   * an agent-scope store (sc1) is written through this XCD's L2 to the
+//     device coherence point, and its vmcnt completes only once it is there;
+//   * the publishing wave waits for that completion (s_waitcnt 0) before its
+//     ticket, an agent-scope atomic performed at the coherence point;
+//   * an agent-scope load (sc1) is served from the coherence point, never
+//     from a stale line of the reader's L2, and the sampler issues its loads
+//     only after its own ticket returned the last count (after the other
+//     publishers' tickets, hence after their stores completed).
+// Only the masses (and a leaf's chunk statistics) cross, all written and
+// read this way.  A release/acquire ticket would write back and invalidate
+// the whole L2 of the XCD at every work-group's hand-over; measured, that
+// lengthens the ragged GQA step from 182 to 222 us, since the attention
+// running beside the acceptance loses its L2 every time.
 __device__ __forceinline__ void store_dev(double* p, double v) {
   __hip_atomic_store(reinterpret_cast<unsigned long long*>(p), __double_as_longlong(v), __ATOMIC_RELAXED,
                      __HIP_MEMORY_SCOPE_AGENT);

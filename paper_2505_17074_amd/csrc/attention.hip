@@ -14,6 +14,17 @@
 namespace sv {
 namespace {
 
+// Diagnostic builds only (-DSV_ATTN_TRACE): per work-group timestamps of the
+// bf16 split kernel on the device's constant-rate clock (start, first tile
+// landed, stream done, end), its hardware placement and its key count, kept
+// in registers and written at the end (a store inside the ring loop would
+// count among the ring's outstanding transfers), read back by
+// sv_attn_trace_copy.
+#ifdef SV_ATTN_TRACE
+constexpr int kAttnTraceBlocks = 65536;
+__device__ unsigned long long g_attn_trace[kAttnTraceBlocks][6];
+#endif
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -473,6 +484,9 @@ void attn_split_mfma(AttnParams p) {
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c16 = lane & 15, grp = lane >> 4;
+#ifdef SV_ATTN_TRACE
+  unsigned long long tr_start = wall_clock64(), tr_first = 0, tr_done = 0;
+#endif
   const AttnItem it = p.items[blockIdx.x];
   mirror_plan(p);
   const int n = it.nq;
@@ -614,12 +628,18 @@ void attn_split_mfma(AttnParams p) {
       if (t + NS - 2 < ntiles) wait_vm<PER * (NS - 2)>();
       else wait_vm<0>();
       ring_barrier();                 // everyone's have landed; stage (t-1) % NS is free
+#ifdef SV_ATTN_TRACE
+      if (t == 0) tr_first = wall_clock64();
+#endif
       if (t + NS - 1 < ntiles) issue(lds + ((st + NS - 1) % NS) * G::STAGE, t + NS - 1, pg_next);
       if (active) compute_tile<D, st * G::STAGE>(lds, S, it.kb + 32 * t, it.ke, ctx, p.scale_log2, lane);
     });
   }
   wait_vm<0>();
   __syncthreads();                    // ring no longer read: reuse it for the output
+#ifdef SV_ATTN_TRACE
+  tr_done = wall_clock64();
+#endif
 
   // row sums across the four lane groups; stage O^T into row-major LDS
   float l = S.l;
@@ -667,15 +687,30 @@ void attn_split_mfma(AttnParams p) {
       *reinterpret_cast<float4*>(dst) = v;
     }
   }
+#ifdef SV_ATTN_TRACE
+  if (threadIdx.x == 0 && blockIdx.x < kAttnTraceBlocks) {
+    unsigned hw = 0, xcc = 0;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    g_attn_trace[blockIdx.x][0] = tr_start;
+    g_attn_trace[blockIdx.x][1] = tr_first;
+    g_attn_trace[blockIdx.x][2] = tr_done;
+    g_attn_trace[blockIdx.x][3] = wall_clock64();
+    g_attn_trace[blockIdx.x][4] = ((unsigned long long)xcc << 32) | hw;
+    g_attn_trace[blockIdx.x][5] = (unsigned long long)(it.ke - it.kb);
+  }
+#endif
   if (publish) {
     // Check in on the stream's counter once this work-group's partial stores
     // have completed; the stream's last piece combines.
-    __shared__ int s_last;
+    // (the flag lives in the ring's LDS, read by no one after the stores above)
+    volatile int* s_last = reinterpret_cast<volatile int*>(lds);
     wait_vm<0>();
     __syncthreads();
-    if (threadIdx.x == 0) s_last = arrive_last(p.counters + it.stream, p.call_tag, it.nseg) ? 1 : 0;
+    if (threadIdx.x == 0) *s_last = arrive_last(p.counters + it.stream, p.call_tag, it.nseg) ? 1 : 0;
     __syncthreads();
-    if (!s_last) return;
+    if (!*s_last) return;
+    __syncthreads();                  // everyone has read the flag before the combine reuses the LDS
     combine_stream<D>(p, it, lds);
   }
 #endif
@@ -872,6 +907,12 @@ hipError_t launch_mfma(const AttnParams& p, int nr, hipStream_t s) {
 }
 
 }  // namespace
+
+#ifdef SV_ATTN_TRACE
+extern "C" __attribute__((visibility("default"))) int sv_attn_trace_copy(void* dst, size_t bytes) {
+  return (int)hipMemcpyFromSymbol(dst, HIP_SYMBOL(g_attn_trace), bytes);
+}
+#endif
 
 int max_rows_per_item(int dtype_bf16, int D) { return dtype_bf16 ? 80 : 4096 / D; }
 
