@@ -105,6 +105,31 @@ __device__ __forceinline__ void load_vec(const T* row, int v, int V, float pad, 
   }
 }
 
+// One 16-byte word of a row as stored (VW entries; entries past V hold
+// pad's bit pattern), and entry e of such a word.
+template <typename T>
+__device__ __forceinline__ uint4 load_raw(const T* row, int v, int V, float pad) {
+  constexpr int VW = 16 / sizeof(T);
+  if (v + VW <= V) return *reinterpret_cast<const uint4*>(row + v);
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int e = 0; e < VW; ++e) {
+    const uint32_t b = __float_as_uint(v + e < V ? ld(row, v + e) : pad);
+    if constexpr (sizeof(T) == 4) w[e] = b;
+    else w[e >> 1] |= (b >> 16) << (16 * (e & 1));
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+template <typename T>
+__device__ __forceinline__ float entry(const uint4& r, int e) {
+  if constexpr (sizeof(T) == 4) {
+    return __uint_as_float(e == 0 ? r.x : e == 1 ? r.y : e == 2 ? r.z : r.w);
+  } else {
+    const uint32_t w = (e >> 1) == 0 ? r.x : (e >> 1) == 1 ? r.y : (e >> 1) == 2 ? r.z : r.w;
+    return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+}
+
 // load_vec with the row-statistics kernel's cache policy.
 template <typename T>
 __device__ __forceinline__ void load_vec_rs(const T* row, int v, int V, float pad, float* out) {
@@ -606,19 +631,35 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
 }
 
 // Sequential sibling verification over a token tree (SpecInfer's multi-step
-// speculative sampling), one 1024-thread work-group per request.  At the
-// current node the children (BFS order) are tested against a running target
-// distribution p', evaluated per token as
+// speculative sampling), C 1024-thread work-groups per request, each holding
+// a contiguous slice of the vocabulary (whole 1024 x VW-entry chunks).  At
+// the current node the children (BFS order) are tested against a running
+// target distribution p', evaluated per token as
 //   p'_0(v) = exp(l(v) - M) / Z,   p'_{j+1}(v) = max(0, p'_j(v) - q(v)) / S_{j+1},
-// where S_{j+1} is the vocabulary sum of max(0, p'_j - q), taken by one
-// coalesced fp64 pass (16-byte loads, several chunks in flight) after each
-// rejection and applied as its reciprocal (within an ulp of the division);
-// a zero sum, reachable only through rounding, leaves p' as it is.  Each
-// child's test inputs (token, the parent row's logit and draft probability
-// there, uniform) do not depend on the walk and are loaded up front.  The first accepted
-// child becomes the current node; when none is, or the node is a leaf, the
-// final token is the smallest id whose cumulative p' exceeds u * (its total).
+// where S_{j+1} is the vocabulary sum of max(0, p'_j - q): each work-group
+// takes its slice's part in one coalesced fp64 pass (16-byte loads, several
+// chunks in flight), and the parts are exchanged (below) and added in slice
+// order, so every work-group holds the same S and takes the same decisions;
+// S is applied as its reciprocal (within an ulp of the division), and a zero
+// sum, reachable only through rounding, leaves p' as it is.  Each child's
+// test inputs (token, the parent row's logit and draft probability there,
+// uniform) do not depend on the walk and are loaded up front.  The first
+// accepted child becomes the current node; when none is, or the node is a
+// leaf, the final token is the smallest id whose cumulative p' exceeds u *
+// (its total): the slices' totals are exchanged, and the work-group whose
+// slice holds the target scans it and writes the outputs.
+//
+// Exchange j of a request: each work-group writes its value with an
+// agent-scope store, waits for it to complete, adds one to the request's
+// counter (cleared by the row-statistics kernel before this launch), and
+// waits until the counter reaches (j + 1) C before reading the C values
+// with agent-scope loads (the acceptance's hand-over argument).  The
+// request's work-groups are consecutive in the grid and dispatched in order,
+// so every one the waiters depend on is resident or already dispatched ahead
+// of them (a CPU model of the protocol checks this).  The wait is bounded:
+// past kSeqSpinLimit polls the work-group gives up and writes -1 outputs.
 constexpr int kSeqThreads = 1024;
+constexpr int kSeqSpinLimit = 1 << 18;
 
 template <int NW>
 __device__ __forceinline__ double block_sum_n(double x, double* red) {
@@ -631,30 +672,96 @@ __device__ __forceinline__ double block_sum_n(double x, double* red) {
   return s;
 }
 
+// U block-wide fp64 sums at once (one pair of barriers), each in a fixed order.
+template <int NW, int U>
+__device__ __forceinline__ void block_sum_u(double (&x)[U], double* red) {
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    for (int o = 32; o >= 1; o >>= 1) x[u] += __shfl_xor(x[u], o);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0)
+#pragma unroll
+    for (int u = 0; u < U; ++u) red[u * NW + (threadIdx.x >> 6)] = x[u];
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    double s = 0.0;
+    for (int w = 0; w < NW; ++w) s += red[u * NW + w];
+    x[u] = s;
+  }
+}
+
+// Exchange j of request i among its C work-groups: this one's (x, y) in,
+// all C pairs out (in LDS, valid after the call for every thread).  Returns
+// false if the wait gave up.
+__device__ __forceinline__ bool seq_exchange(const AccParams& p, int i, int c, int C, int j, double x, int y,
+                                             double* xs, int* ys, int* s_ok) {
+  if (C == 1) {
+    if (threadIdx.x == 0) {
+      xs[0] = x;
+      ys[0] = y;
+    }
+    __syncthreads();
+    return true;
+  }
+  if (threadIdx.x == 0) {
+    SeqSlot* base = p.seq_slots + ((int64_t)i * kMaxNodes + j) * C;
+    store_dev(&base[c].x, x);
+    __hip_atomic_store(&base[c].y, y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_waitcnt(0);     // both stores have reached the device coherence point
+    __hip_atomic_fetch_add(p.tickets + i, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int want = (j + 1) * C;
+    int ok = 1;
+    for (int spins = 0; __hip_atomic_load(p.tickets + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < want;) {
+      __builtin_amdgcn_s_sleep(2);
+      if (++spins > kSeqSpinLimit) {
+        ok = 0;
+        break;
+      }
+    }
+    for (int cc = 0; cc < C; ++cc) {
+      xs[cc] = load_dev(&base[cc].x);
+      ys[cc] = __hip_atomic_load(&base[cc].y, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    *s_ok = ok;
+  }
+  __syncthreads();
+  return *s_ok != 0;
+}
+
 template <typename T>
 __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
   constexpr int NW = kSeqThreads / 64;
   constexpr int VW = 16 / sizeof(T);            // entries per 16-byte load
   constexpr int CH = kSeqThreads * VW;          // entries per chunk
-  constexpr int UNR = 16 / VW;                  // chunks whose loads are in flight together (16 entries)
+  constexpr int UNR = 2;                        // chunks whose loads are in flight together
   __shared__ float s_M[kMaxNodes];
   __shared__ double s_Z[kMaxNodes];
   __shared__ double s_iS[kMaxNodes];           // 1 / S_j at the current node
   __shared__ float s_lx[kMaxNodes], s_qx[kMaxNodes], s_u[kMaxNodes];
   __shared__ double redd[NW];
+  __shared__ double s_redu[NW * 4];              // U <= 4 sums at once (UNR and the resident RES)
+  __shared__ int s_v;
   __shared__ double s_chunk[kAccMaxChunks * kAccChunk / (kSeqThreads * 4)];
-  __shared__ double s_tsum[kSeqThreads];
   __shared__ double s_wtot[NW];
   __shared__ double s_run, s_target;
   __shared__ int s_pos[NW];
   __shared__ int s_pick;
   __shared__ int s_par[kMaxNodes], s_dep[kMaxNodes], s_qr[kMaxNodes];
-  const int i = blockIdx.x;
+  __shared__ double s_xs[kSeqMaxGroups];
+  __shared__ int s_ys[kSeqMaxGroups];
+  __shared__ int s_ok;
+  SV_TRACE(1, 0);
+  const int C = p.seq_groups;
+  const int i = blockIdx.x / C, c = blockIdx.x % C;
   const int tid = threadIdx.x, wv = tid >> 6, ln = tid & 63;
   const ReqInfo rq = p.reqs[i];
   const int N = rq.nq;
   const T* L = static_cast<const T*>(p.logits);
   const T* Q = static_cast<const T*>(p.probs);
+  // this work-group's chunks [ch0, ch1) of the vocabulary
+  const int nchunk = (p.V + CH - 1) / CH;
+  const int ch0 = (int)((int64_t)c * nchunk / C), ch1 = (int)((int64_t)(c + 1) * nchunk / C);
 
   // every child's test inputs, which do not depend on the walk: its token,
   // its parent's logit and draft probability there, and its uniform
@@ -685,13 +792,21 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
     }
   }
   __syncthreads();
+  SV_TRACE(1, 1);
 
-  int node = 0, k = 0;                         // current node, rejections at it (uniform)
+  int node = 0, k = 0, xj = 0;                 // current node, rejections at it, exchanges so far (uniform)
   const T* Lr = L;
   const T* Qr = Q;
   bool has_q = false;
   float M = 0.f;
   double invZ = 1.0;
+  auto give_up = [&]() {
+    if (tid == 0 && c == 0) {
+      p.acc_len[i] = -1;
+      p.next_tok[i] = -1;
+      if (p.acc_node) p.acc_node[i] = -1;
+    }
+  };
   // running distribution at a token from its logit l and draft probability q
   auto prun = [&](float l, float q) -> double {
     double x = (double)exp_rel(l, M) * invZ;
@@ -706,6 +821,27 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
     else
       for (int e = 0; e < VW; ++e) q[e] = 0.f;
   };
+  // A slice of at most RES chunks stays in registers while the walk is at a
+  // node: loaded as the node is entered (in flight during its first test),
+  // it serves every normaliser pass and the final sample there; longer
+  // slices, and bf16 rows (whose unpacked entries would not fit the register
+  // budget), are streamed per pass.  Both read the entries in the same order.
+  constexpr int RES = 2;
+  const bool resident = sizeof(T) == 4 && ch1 - ch0 <= RES;
+  uint4 rl[RES], rqv[RES];
+#pragma unroll
+  for (int r = 0; r < RES; ++r) rl[r] = rqv[r] = make_uint4(0u, 0u, 0u, 0u);
+  auto load_resident = [&]() {
+    if (!resident) return;
+#pragma unroll
+    for (int r = 0; r < RES; ++r) {
+      if (ch0 + r < ch1) {
+        const int v = (ch0 + r) * CH + tid * VW;
+        rl[r] = load_raw(Lr, v, p.V, -INFINITY);
+        rqv[r] = has_q ? load_raw(Qr, v, p.V, 0.f) : make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+  };
   for (;;) {
     M = s_M[node];
     invZ = 1.0 / s_Z[node];
@@ -713,28 +849,53 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
     const int qr = s_qr[node];
     has_q = qr >= 0;
     Qr = Q + (int64_t)(rq.d0 + (has_q ? qr : 0)) * p.p_st;
+    load_resident();
     k = 0;
     int next = -1;
-    for (int c = node + 1; c < N && next < 0; ++c) {
-      if (s_par[c] != node) continue;
-      const float qx = s_qx[c];
-      const double px = prun(s_lx[c], qx);
-      if ((double)s_u[c] * (double)qx < px) {
-        next = c;
+    for (int cn = node + 1; cn < N && next < 0; ++cn) {
+      if (s_par[cn] != node) continue;
+      const float qx = s_qx[cn];
+      const double px = prun(s_lx[cn], qx);
+      if ((double)s_u[cn] * (double)qx < px) {
+        next = cn;
         break;
       }
-      // rejected: the normaliser of max(0, p' - q), UNR chunks' loads in flight
+      // rejected: this slice's part of the normaliser of max(0, p' - q),
+      // UNR chunks' loads in flight, then the parts of all slices
       double part = 0.0;
-      for (int b = 0; b < p.V; b += CH * UNR) {
+      if (resident) {
+#pragma unroll
+        for (int r = 0; r < RES; ++r)
+          if (ch0 + r < ch1)
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+              const float q = entry<T>(rqv[r], e);
+              part += fmax(0.0, prun(entry<T>(rl[r], e), q) - (double)q);
+            }
+      }
+      for (int b = ch0 * CH; !resident && b < ch1 * CH; b += CH * UNR) {
         float l[UNR][VW], q[UNR][VW];
 #pragma unroll
-        for (int u = 0; u < UNR; ++u) load(b + u * CH + tid * VW, l[u], q[u]);
+        for (int u = 0; u < UNR; ++u) {
+          if (b + u * CH < ch1 * CH) {
+            load(b + u * CH + tid * VW, l[u], q[u]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+              l[u][e] = -INFINITY;
+              q[u][e] = 0.f;
+            }
+          }
+        }
 #pragma unroll
         for (int u = 0; u < UNR; ++u)
 #pragma unroll
           for (int e = 0; e < VW; ++e) part += fmax(0.0, prun(l[u][e], q[u][e]) - (double)q[u][e]);
       }
-      const double S = block_sum_n<NW>(part, redd);
+      part = block_sum_n<NW>(part, redd);
+      if (!seq_exchange(p, i, c, C, xj++, part, 0, s_xs, s_ys, &s_ok)) return give_up();
+      double S = 0.0;
+      for (int cc = 0; cc < C; ++cc) S += s_xs[cc];
       if (S > 0.0) {
         if (tid == 0) s_iS[k] = 1.0 / S;
         __syncthreads();
@@ -744,17 +905,49 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
     if (next < 0) break;
     node = next;
   }
+  SV_TRACE(1, 2);
 
-  // The final token from p' at `node`.  Chunk totals (block sums) and the
-  // last id with positive weight first; then one thread walks the chunk
-  // totals, the chosen chunk's per-thread sums and that thread's entries in
-  // token order, so every boundary comes from one sequence of fp64 sums.
-  const int nchunk = (p.V + CH - 1) / CH;
+  // The final token from p' at `node`.  This slice's chunk totals (block
+  // sums) and its last id with positive weight; the slices' totals and last
+  // ids exchanged; the slice holding u * total (its running sum from the
+  // slices before it) walks its chunk totals, the chosen chunk's per-thread
+  // sums and that thread's entries in token order, so every boundary comes
+  // from one sequence of fp64 sums.
   int last = -1;
-  for (int c0 = 0; c0 < nchunk; c0 += UNR) {
+  if (resident) {
+    double part[RES];
+#pragma unroll
+    for (int r = 0; r < RES; ++r) {
+      part[r] = 0.0;
+      if (ch0 + r < ch1)
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+          const double w = prun(entry<T>(rl[r], e), entry<T>(rqv[r], e));
+          part[r] += w;
+          if (w > 0.0) last = (ch0 + r) * CH + tid * VW + e;
+        }
+    }
+    block_sum_u<NW, RES>(part, s_redu);
+    if (tid == 0)
+#pragma unroll
+      for (int r = 0; r < RES; ++r)
+        if (ch0 + r < ch1) s_chunk[ch0 + r] = part[r];
+    __syncthreads();
+  }
+  for (int c0 = ch0; !resident && c0 < ch1; c0 += UNR) {
     float l[UNR][VW], q[UNR][VW];
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) load((c0 + u) * CH + tid * VW, l[u], q[u]);
+    for (int u = 0; u < UNR; ++u) {
+      if (c0 + u < ch1) {
+        load((c0 + u) * CH + tid * VW, l[u], q[u]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+          l[u][e] = -INFINITY;
+          q[u][e] = 0.f;
+        }
+      }
+    }
     double part[UNR];
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
@@ -766,72 +959,115 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
         if (w > 0.0) last = (c0 + u) * CH + tid * VW + e;
       }
     }
+    block_sum_u<NW, UNR>(part, s_redu);
+    if (tid == 0)
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const double tot = block_sum_n<NW>(part[u], redd);
-      if (tid == 0 && c0 + u < nchunk) s_chunk[c0 + u] = tot;
-    }
+      for (int u = 0; u < UNR; ++u)
+        if (c0 + u < ch1) s_chunk[c0 + u] = part[u];
+    __syncthreads();                   // s_redu is reused by the next pass
   }
   for (int o = 32; o >= 1; o >>= 1) last = max(last, __shfl_xor(last, o));
   if (ln == 0) s_pos[wv] = last;
   __syncthreads();
+  SV_TRACE(1, 3);
+  double slice = 0.0;
+  int slice_last = -1;
   if (tid == 0) {
-    double total = 0.0;
-    for (int ch = 0; ch < nchunk; ++ch) total += s_chunk[ch];
-    const double target = (double)p.uniforms[rq.q0 + N - 1] * total;
-    double run = 0.0;
-    int pick = -1;
-    for (int ch = 0; ch < nchunk && pick < 0; ++ch) {
-      if (run + s_chunk[ch] > target) pick = ch;
-      else run += s_chunk[ch];
+    for (int ch = ch0; ch < ch1; ++ch) slice += s_chunk[ch];
+    for (int w = 0; w < NW; ++w) slice_last = max(slice_last, s_pos[w]);
+  }
+  if (!seq_exchange(p, i, c, C, xj++, slice, slice_last, s_xs, s_ys, &s_ok)) return give_up();
+  // the slice that holds the target writes the outputs; if none does (the
+  // target rounded to or past the total), the last slice with positive weight
+  // writes its last such id
+  double total = 0.0;
+  for (int cc = 0; cc < C; ++cc) total += s_xs[cc];
+  const double target = (double)p.uniforms[rq.q0 + N - 1] * total;
+  int owner = -1, fallback = -1;
+  double before = 0.0, before_owner = 0.0;
+  for (int cc = 0; cc < C; ++cc) {
+    if (owner < 0 && s_xs[cc] > 0.0 && before + s_xs[cc] > target) {
+      owner = cc;
+      before_owner = before;
     }
+    before += s_xs[cc];
+    if (s_ys[cc] >= 0) fallback = cc;
+  }
+  const int writer = owner >= 0 ? owner : (fallback >= 0 ? fallback : 0);
+  SV_TRACE(1, 4);
+  if (c != writer) return;
+  if (tid == 0) {
+    const double t = target;
+    double run = owner >= 0 ? before_owner : 0.0;
+    int pick = -1;
+    if (owner >= 0)
+      for (int ch = ch0; ch < ch1 && pick < 0; ++ch) {
+        if (run + s_chunk[ch] > t) pick = ch;
+        else run += s_chunk[ch];
+      }
     s_pick = pick;
     s_run = run;
-    s_target = target;
+    s_target = t;
   }
   __syncthreads();
-  int v = -1;
+  SV_TRACE(1, 5);
+  // Inside the chosen chunk: each thread's sum of its VW entries, a prefix
+  // over the threads (a scan in each wave, then the waves' totals), and the
+  // thread whose range holds the target scans its own entries.
+  if (tid == 0) s_v = -1;
   if (s_pick >= 0) {
-    {
-      const int vb = s_pick * CH + tid * VW;
-      float l[VW], q[VW];
-      load(vb, l, q);
-      double part = 0.0;
+    const int vb = s_pick * CH + tid * VW;
+    float l[VW], q[VW];
+    if (resident) {
+      const int pr = s_pick - ch0;
 #pragma unroll
-      for (int e = 0; e < VW; ++e) part += prun(l[e], q[e]);
-      s_tsum[tid] = part;
-    }
-    __syncthreads();
-    if (ln == 0) {                           // each wave's total, in lane order
-      double w = 0.0;
-      for (int t = 0; t < 64; ++t) w += s_tsum[wv * 64 + t];
-      s_wtot[wv] = w;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      const double target = s_target;
-      double c = s_run;
-      int w = 0;
-      while (w < NW - 1 && !(c + s_wtot[w] > target)) c += s_wtot[w++];
-      int t = w * 64;
-      while (t < w * 64 + 63 && !(c + s_tsum[t] > target)) c += s_tsum[t++];
-      const int vb = s_pick * CH + t * VW;
-      float l[VW], q[VW];
+      for (int r = 0; r < RES; ++r)
+        if (r == pr)
+#pragma unroll
+          for (int e = 0; e < VW; ++e) {
+            l[e] = entry<T>(rl[r], e);
+            q[e] = entry<T>(rqv[r], e);
+          }
+    } else {
       load(vb, l, q);
+    }
+    double w[VW];
+    double part = 0.0;
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+      w[e] = prun(l[e], q[e]);
+      part += w[e];
+    }
+    double incl = part;
+    for (int o = 1; o < 64; o <<= 1) {
+      const double y = __shfl_up(incl, o);
+      if (ln >= o) incl += y;
+    }
+    if (ln == 63) s_wtot[wv] = incl;
+    __syncthreads();
+    double cum = s_run;
+    for (int ww = 0; ww < wv; ++ww) cum += s_wtot[ww];
+    cum += incl - part;                   // before this thread's entries
+    const double t = s_target;
+    if (part > 0.0 && cum <= t && cum + part > t) {   // at most one thread
+      int v = -1;
       for (int e = 0; e < VW && v < 0; ++e) {
-        c += prun(l[e], q[e]);
-        if (c > target) v = vb + e;
+        cum += w[e];
+        if (cum > t) v = vb + e;
       }
+      s_v = v;
     }
   }
+  __syncthreads();
+  int v = s_v;
   if (tid == 0) {
-    // a target at or past the total (rounding): the last id with positive weight
-    if (v < 0)
-      for (int w = 0; w < NW; ++w) v = max(v, s_pos[w]);
+    // a target at or past this slice's total (rounding): its last id with positive weight
+    if (v < 0) v = s_ys[c];
     p.acc_len[i] = s_dep[node];
     p.next_tok[i] = v;
     if (p.acc_node) p.acc_node[i] = node;
   }
+  SV_TRACE(1, 7);
 }
 
 // One work-group: every request's draft tokens, their draft probabilities
@@ -928,8 +1164,9 @@ hipError_t launch_rowstats(const AccParams& p, hipStream_t s) {
 hipError_t launch_decide(const AccParams& p, hipStream_t s) {
   dim3 block(kAccThreads);
   if (p.tree == 2) {                       // sequential sibling verification
-    if (p.bf16) acc_tree_seq<uint16_t><<<dim3(p.B), dim3(kSeqThreads), 0, s>>>(p);
-    else acc_tree_seq<float><<<dim3(p.B), dim3(kSeqThreads), 0, s>>>(p);
+    const dim3 grid((unsigned)(p.B * p.seq_groups));
+    if (p.bf16) acc_tree_seq<uint16_t><<<grid, dim3(kSeqThreads), 0, s>>>(p);
+    else acc_tree_seq<float><<<grid, dim3(kSeqThreads), 0, s>>>(p);
     return hipGetLastError();
   }
   if (p.bf16) acc_decide_select<uint16_t><<<dim3(p.B * p.nch), block, 0, s>>>(p);

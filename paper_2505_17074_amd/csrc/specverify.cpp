@@ -50,7 +50,7 @@ struct Plan {
   int nch = 0;
   // layout (bytes)
   size_t off_reqs = 0, off_rowreq = 0, off_items = 0, off_nodes = 0, plan_bytes = 0;
-  size_t off_acc_reqs = 0, off_acc_nodes = 0, off_tickets = 0;
+  size_t off_acc_reqs = 0, off_acc_nodes = 0, off_tickets = 0, off_seq = 0;
   size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_masses = 0, off_flag = 0, off_counters = 0;
   size_t device_bytes = 0;
 };
@@ -500,6 +500,8 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   off = align_up(off + sizeof(sv::NodeInfo) * (P.has_acc ? P.nodes.size() : 0));
   P.off_tickets = off;                 // acceptance tickets, cleared on the device
   off = align_up(off + sizeof(int32_t) * (size_t)(P.has_acc ? P.B : 0));
+  P.off_seq = off;                     // sequential sibling rule: exchange slots
+  off = align_up(off + sizeof(sv::SeqSlot) * sv::kMaxNodes * sv::kSeqMaxGroups * (size_t)(P.has_acc && P.tree ? P.B : 0));
   const int D = attn ? attn->head_dim : 0;
   P.off_part_o = off;
   off = align_up(off + sizeof(float) * (size_t)P.parts * D);
@@ -718,6 +720,17 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     c.per_req = P.per_req ? 1 : 0;
     c.nodes_n16 = (int32_t)((sizeof(sv::NodeInfo) * P.nodes.size() + 15) / 16);
     c.all_stats = (P.per_req || mode.lm) ? 1 : 0;
+    // sequential sibling rule: work-groups per request, enough to give every
+    // compute unit one, at most kSeqMaxGroups and at most the 1024-thread
+    // chunks of the vocabulary
+    {
+      const int64_t ch = 1024 * (acc->dtype == SPEC_BF16 ? 8 : 4);
+      const int64_t nchunk = (acc->vocab + ch - 1) / ch;
+      int64_t g = device_cus() / std::max(P.B, 1);
+      g = std::min<int64_t>(std::min<int64_t>(g, sv::kSeqMaxGroups), nchunk);
+      c.seq_groups = (int32_t)std::max<int64_t>(g, 1);
+      c.seq_slots = reinterpret_cast<sv::SeqSlot*>(d + P.off_seq);
+    }
   }
 
   // Optional device check of the acceptance inputs (the caller's contract),

@@ -126,6 +126,15 @@ struct ChunkStat {
   float pad;
 };
 
+// One value a work-group of the sequential sibling kernel hands the other
+// work-groups of its request at one exchange.
+struct SeqSlot {
+  double x;
+  int32_t y;
+  int32_t pad;
+};
+constexpr int kSeqMaxGroups = 8;       // work-groups per request, at most
+
 // Per request: the accepted node, the row the final token is drawn from, its
 // draft row (-1: the extra token is drawn from p itself) and normaliser.
 struct Decision {
@@ -162,7 +171,10 @@ struct AccParams {
   int32_t per_req;
   int32_t nodes_n16;
   int32_t all_stats;   // every row has chunk statistics before the decision kernel runs
-  int32_t pad1;
+  // sequential sibling rule: work-groups per request, and their exchange
+  // slots [B, kMaxNodes, seq_groups]
+  int32_t seq_groups;
+  SeqSlot* seq_slots;
 };
 
 constexpr int kAccMaxChunks = 1024;    // vocabularies up to 4M entries
