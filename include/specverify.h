@@ -234,6 +234,11 @@ typedef struct spec_attn_args {
  *     mass).  The first accepted child becomes the current node; when none
  *     is, or the node is a leaf, the final token is drawn from p'.
  *     accepted_node is the last current node, accepted_len its depth.
+ *     Each request's walk runs on up to 8 work-groups that split the
+ *     vocabulary (one per compute unit when there are few requests); the
+ *     environment variable SPEC_SEQ_GROUPS (1..8) fixes that number.  Their
+ *     waits on each other are bounded: a request whose wait gives up (not
+ *     expected in any normal run) gets -1 in all three outputs.
  * Inverse-CDF convention: token ids ascending, the smallest id whose
  * cumulative weight exceeds u * (total weight); zero weights never chosen.
  */

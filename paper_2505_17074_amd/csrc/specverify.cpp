@@ -727,6 +727,12 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
       const int64_t ch = 1024 * (acc->dtype == SPEC_BF16 ? 8 : 4);
       const int64_t nchunk = (acc->vocab + ch - 1) / ch;
       int64_t g = device_cus() / std::max(P.B, 1);
+      // SPEC_SEQ_GROUPS (1..8) replaces the choice (the tests use it to run
+      // every split of the vocabulary)
+      if (const char* e = std::getenv("SPEC_SEQ_GROUPS")) {
+        const long v = std::strtol(e, nullptr, 10);
+        if (v >= 1 && v <= sv::kSeqMaxGroups) g = v;
+      }
       g = std::min<int64_t>(std::min<int64_t>(g, sv::kSeqMaxGroups), nchunk);
       c.seq_groups = (int32_t)std::max<int64_t>(g, 1);
       c.seq_slots = reinterpret_cast<sv::SeqSlot*>(d + P.off_seq);

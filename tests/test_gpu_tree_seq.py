@@ -104,3 +104,18 @@ def test_first_token_distribution_exact_on_gpu(gpu_lib):
         y = (c[0] if node == 1 else c[1]) if length == 1 else int(out["next_token"][i])
         got[y] += c[5]
     np.testing.assert_allclose(got, p0, rtol=0, atol=1e-6)
+
+
+@pytest.mark.parametrize("groups", [1, 2, 3, 8])
+def test_work_groups_per_request(gpu_lib, monkeypatch, groups):
+    """The walk split over 1, 2, 3 and 8 work-groups per request (uneven
+    slices at 3; 8 slices of one chunk each at the 32000-entry vocabulary),
+    every exchange of normalisers and slice totals through the request's
+    counter, against the oracle."""
+    monkeypatch.setenv("SPEC_SEQ_GROUPS", str(groups))
+    print(f"[case] sequential tree15 b16 seed 5, {groups} work-groups per request", flush=True)
+    _check(W.make_pool(W.CONFIGS[4], 5, batch=16), f"tree15/b16/groups{groups}")
+    seed = U.case_seed("groups_wide_bf16")
+    pool = U.custom_pool(ctx=[10, 20, 30, 40], tree_parent=[-1, 0, 0, 0, 0, 0, 1, 2, 2, 2], V=20000, logit=W.BF16,
+                         seed=seed, sigma=2.0)
+    _check(pool, f"wide/bf16/groups{groups}")
