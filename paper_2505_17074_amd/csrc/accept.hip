@@ -26,6 +26,7 @@
 // The sampled token then follows the exact inverse CDF except where u * S
 // lies within ~1e-8 (probability mass) of a cumulative boundary.
 #include <algorithm>
+#include <climits>
 
 #include "sv_internal.h"
 
@@ -1014,7 +1015,7 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
   // Inside the chosen chunk: each thread's sum of its VW entries, a prefix
   // over the threads (a scan in each wave, then the waves' totals), and the
   // thread whose range holds the target scans its own entries.
-  if (tid == 0) s_v = -1;
+  if (tid == 0) s_v = INT_MAX;
   if (s_pick >= 0) {
     const int vb = s_pick * CH + tid * VW;
     float l[VW], q[VW];
@@ -1049,17 +1050,19 @@ __global__ __launch_bounds__(kSeqThreads) void acc_tree_seq(AccParams p) {
     for (int ww = 0; ww < wv; ++ww) cum += s_wtot[ww];
     cum += incl - part;                   // before this thread's entries
     const double t = s_target;
-    if (part > 0.0 && cum <= t && cum + part > t) {   // at most one thread
+    if (part > 0.0 && cum <= t && cum + part > t) {
+      // one thread in exact arithmetic; should rounding let two ranges
+      // straddle the target, the smaller id wins, whatever their order
       int v = -1;
       for (int e = 0; e < VW && v < 0; ++e) {
         cum += w[e];
         if (cum > t) v = vb + e;
       }
-      s_v = v;
+      if (v >= 0) atomicMin(&s_v, v);
     }
   }
   __syncthreads();
-  int v = s_v;
+  int v = s_v == INT_MAX ? -1 : s_v;
   if (tid == 0) {
     // a target at or past this slice's total (rounding): its last id with positive weight
     if (v < 0) v = s_ys[c];
