@@ -191,9 +191,14 @@ def cpu_model() -> str:
     return "unknown"
 
 
+# The sources the attention kernels are compiled from (the kernels and the two
+# headers they include): counter figures taken on other sources are stale.
+ATTN_SOURCES = ("attention.hip", "sv_attn.h", "sv_common.h")
+
+
 def kernel_source_digest() -> str:
     h = hashlib.sha256()
-    for name in ("attention.hip", "sv_internal.h"):
+    for name in ATTN_SOURCES:
         with open(os.path.join(ROOT, "paper_2505_17074_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]

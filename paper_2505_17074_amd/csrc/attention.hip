@@ -6,7 +6,7 @@
 // its own ancestors-or-self inside the verify block (causal for a chain).
 // Scores and the online softmax run in fp32; the running max is kept in log2
 // units (scores pre-multiplied by scale * log2 e) so exp2 is one v_exp_f32.
-#include "sv_internal.h"
+#include "sv_attn.h"
 
 #include <algorithm>
 #include <type_traits>
