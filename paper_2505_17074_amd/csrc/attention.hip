@@ -169,10 +169,15 @@ __device__ __forceinline__ void ring_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// A tile's transfers are dealt round-robin over the waves: wave w issues
+// transfers w, w + W, ... < NI, PER of them when w < FULL, else PER - 1 (an
+// uneven split issues no padding transfer; each wave waits on its own count).
 template <int D, int W>
 struct Xfer {
   static constexpr int NI = 2 * Geo<D>::IPM;        // transfers per tile (K then V)
-  static constexpr int PER = (NI + W - 1) / W;      // per wave (padded with repeats)
+  static constexpr int PER = (NI + W - 1) / W;      // per wave, at most
+  static constexpr int FULL = NI - (PER - 1) * W;   // waves that issue PER
+  static constexpr bool EVEN = NI % W == 0;         // every wave issues PER
 };
 
 // Byte offset, inside a tile, of the global chunk lane `lane` moves in
@@ -196,8 +201,7 @@ struct XferPlan {
 // Wave w's transfers of the tile starting at key t0 into `stage`, as
 // buffer_load_dwordx4 ... lds with the tile start in soffset and each lane's
 // precomputed offset in voffset.  Tiles that reach past ke clamp their rows
-// to ke - 1 (in bounds, masked later); the pad transfers of uneven splits
-// repeat an earlier one with identical data.
+// to ke - 1 (in bounds, masked later).
 template <int D, int W>
 __device__ __forceinline__ void issue_tile(char* stage, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv,
                                            int row_bytes, int t0, int ke, int w, int lane,
@@ -207,7 +211,9 @@ __device__ __forceinline__ void issue_tile(char* stage, __amdgpu_buffer_rsrc_t r
     const uint32_t soff = (uint32_t)t0 * (uint32_t)row_bytes;
 #pragma unroll
     for (int q = 0; q < Xfer<D, W>::PER; ++q) {
-      const int j = (w + q * W) % Xfer<D, W>::NI;
+      if constexpr (!Xfer<D, W>::EVEN)
+        if (w + q * W >= Xfer<D, W>::NI) break;     // wave-uniform: this wave's last is done
+      const int j = w + q * W;
       const bool isv = j >= G::IPM;
       const int jj = isv ? j - G::IPM : j;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(isv ? rv : rk, (lds_void_t*)(stage + (isv ? G::MAT : 0) + jj * 1024),
@@ -216,7 +222,9 @@ __device__ __forceinline__ void issue_tile(char* stage, __amdgpu_buffer_rsrc_t r
   } else {
 #pragma unroll
     for (int q = 0; q < Xfer<D, W>::PER; ++q) {
-      const int j = (w + q * W) % Xfer<D, W>::NI;
+      if constexpr (!Xfer<D, W>::EVEN)
+        if (w + q * W >= Xfer<D, W>::NI) break;     // wave-uniform: this wave's last is done
+      const int j = w + q * W;
       const bool isv = j >= G::IPM;
       const int jj = isv ? j - G::IPM : j;
       int row;
@@ -586,14 +594,17 @@ void attn_split_mfma(AttnParams p) {
   const bool active = w * 16 < R;     // wave-uniform: this wave has query rows
 
   // The ring's first NS-1 tiles, issued whatever the item's length so that
-  // every wave has the same transfer count behind its query loads (a tile
+  // the transfer count behind each wave's query loads is fixed (a tile
   // past the item's end re-reads its last key row, in bounds, and is never
   // computed).  The query loads are older than these transfers: wait for them
   // alone, and hand the registers through an empty asm so that no later use
   // inherits a wait on the ring.
 #pragma unroll
   for (int st = 0; st < NS - 1; ++st) issue(lds + st * G::STAGE, st, PG ? page_of(st) : 0);
-  wait_vm<PER * (NS - 1)>();
+  // this wave's transfers per tile: PER, or PER - 1 on the last waves of an uneven split
+  const bool full_wave = Xfer<D, W>::EVEN || w < Xfer<D, W>::FULL;
+  if (full_wave) wait_vm<PER * (NS - 1)>();
+  else wait_vm<(PER - 1) * (NS - 1)>();
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(S.q[ks]));
   if (p.per_req) {
@@ -625,8 +636,9 @@ void attn_split_mfma(AttnParams p) {
       const int pg_next = (PG && t + NS - 1 < ntiles) ? page_of(t + NS - 1) : 0;
       // this wave's transfers of tile t have landed: NS-2 later tiles may still
       // be in flight, none in the item's last NS-2 tiles (over-waiting there)
-      if (t + NS - 2 < ntiles) wait_vm<PER * (NS - 2)>();
-      else wait_vm<0>();
+      if (t + NS - 2 >= ntiles) wait_vm<0>();
+      else if (full_wave) wait_vm<PER * (NS - 2)>();
+      else wait_vm<(PER - 1) * (NS - 2)>();
       ring_barrier();                 // everyone's have landed; stage (t-1) % NS is free
 #ifdef SV_ATTN_TRACE
       if (t == 0) tr_first = wall_clock64();
