@@ -119,3 +119,34 @@ def test_work_groups_per_request(gpu_lib, monkeypatch, groups):
     pool = U.custom_pool(ctx=[10, 20, 30, 40], tree_parent=[-1, 0, 0, 0, 0, 0, 1, 2, 2, 2], V=20000, logit=W.BF16,
                          seed=seed, sigma=2.0)
     _check(pool, f"wide/bf16/groups{groups}")
+
+
+def test_full_step_beside_the_attention(gpu_lib):
+    """The sequential rule inside spec_verify: its work-groups run on the side
+    stream while the attention's fill the device, so a request's later
+    work-groups may start only as attention work-groups finish (the waits are
+    bounded well past that).  Three calls on one workspace give the oracle's
+    decisions, attention within tolerance, and bit-identical outputs."""
+    print("[case] sequential rule in the full verify step, tree15 full size, seed 0", flush=True)
+    pool = U.full_pool(4)
+    b = DeviceBatch(pool, "cuda")
+    v = Verifier(b)
+    v.acc.tree_rule = B.SPEC_TREE_SEQUENTIAL
+    outs = []
+    for _ in range(3):
+        b.accepted_len.fill_(-7)
+        b.next_token.fill_(-7)
+        v.run("verify")
+        outs.append(v.results())
+    ref = verify_accept(pool.target_logits, pool.draft_probs, pool.draft_tokens, pool.uniforms, pool.n_q,
+                        dtype=pool.logit_dtype, tree_parent=pool.tree_parent, tree_rule="sequential")
+    bad, ties = U.compare_accept(outs[0], ref, pool)
+    print(f"step/sequential B={pool.batch} near_ties={ties} mismatches={bad}", flush=True)
+    assert not bad and ties <= U.max_near_ties(pool.batch)
+    for o in outs[1:]:
+        for key in ("accepted_len", "next_token", "accepted_node"):
+            assert np.array_equal(o[key], outs[0][key]), key
+        assert np.array_equal(o["out"].view(np.uint32), outs[0]["out"].view(np.uint32))
+    sample = [0, pool.batch // 2, pool.batch - 1]
+    r = U.attention_ratios(outs[0]["out"], pool, U.oracle_attention_rows(pool, sample))
+    assert np.isfinite(r).all() and r.max() <= U.ATTN_RTOL
