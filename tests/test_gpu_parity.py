@@ -206,6 +206,13 @@ EDGE = [
     ("gqa_two_waves_d128", dict(ctx=[300, 1200, 40, 5000], k=[5, 7, 3, 7], Hq=8, Hkv=2)),
     ("gqa_two_waves_d64", dict(ctx=[100, 2500], k=[7, 2], Hq=8, Hkv=2, d=64)),
     ("gqa_three_waves_short", dict(ctx=[33, 65, 0], k=[8, 1, 2], Hq=8, Hkv=2)),
+    # uneven wave splits of a tile's transfers (the first waves issue one
+    # more than the rest, each waits on its own count): 3 and 5 waves at
+    # d = 64 (8 transfers a tile) and 5 waves at d = 128 (16), ragged
+    # contexts and a split request
+    ("gqa_three_waves_d64", dict(ctx=[1000, 7, 6100, 95], k=[8, 3, 8, 5], Hq=8, Hkv=2, d=64)),
+    ("gqa_five_waves_d64", dict(ctx=[2500, 41, 9000], k=[8, 8, 2], Hq=16, Hkv=2, d=64)),
+    ("gqa_five_waves_d128", dict(ctx=[3001, 100, 12000, 0], k=[8, 8, 3, 8], Hq=16, Hkv=2)),
 ]
 
 
