@@ -475,6 +475,30 @@ def measure_workload(name: str, seed: int, K: int, Wm: int, dev, flush, settle_s
     torch.cuda.synchronize()
     ver.acc.event_begin = ver.acc.event_end = ver.acc.event_mid = None
     t_rows_us = float(np.mean([ev[k][2].elapsed_time(ev[k][4]) for k in range(K)]) * 1e3)
+    # the acceptance's floor (spec_accept_floor_probe): the rows the row
+    # statistics stream (under the shared-tree independent rule, the rows of
+    # nodes with children), then the decision's chain of dependent round
+    # trips, with none of the arithmetic; cold, like the acceptance above
+    nreq = pool.batch
+    floor_rows = int(pool.n_q.sum())
+    if pool.tree_parent is not None and pool.tree_parents is None:
+        inner = np.zeros(len(pool.tree_parent), bool)
+        inner[np.asarray(pool.tree_parent)[1:]] = True
+        floor_rows = nreq * int(inner.sum())
+    eb = batch.logits.element_size()
+    fws_bytes = B.spec_accept_floor_probe_bytes(pool.vocab, floor_rows, nreq)
+    fws = torch.empty(fws_bytes, dtype=torch.uint8, device=dev)
+    fout = torch.empty(nreq, dtype=torch.int32, device=dev)
+    for k in range(K):
+        flush()
+        ev[k][2].record(stream)
+        st = B.spec_accept_floor_probe(batch.logits.data_ptr(), batch.logits.stride(0), eb, pool.vocab, floor_rows,
+                                       nreq, fws.data_ptr(), fws_bytes, fout.data_ptr(), stream.cuda_stream)
+        B.check(st, "spec_accept_floor_probe")
+        ev[k][3].record(stream)
+    torch.cuda.synchronize()
+    t_floor_us = float(np.mean([ev[k][2].elapsed_time(ev[k][3]) for k in range(K)]) * 1e3)
+    del fws, fout
 
     # the outputs of the last (cold) step stand for every step: same inputs
     ver.run("verify", stream)
@@ -513,7 +537,8 @@ def measure_workload(name: str, seed: int, K: int, Wm: int, dev, flush, settle_s
         "accepted_plus_bonus_tokens_per_s": emitted / (ms * 1e-3),
         "cold": {"steps": KF, "step_us_median": float(np.median(cold)), "step_us_p10": pct(cold, 10),
                  "step_us_p90": pct(cold, 90), "verified_tokens_per_s": work["Nq"] / (float(np.median(cold)) * 1e-6)},
-        "accept": {"kernels_us": t_acc_us, "kernels_us_p10": pct(acc_cold, 10),
+        "accept": {"kernels_us": t_acc_us, "floor_us": t_floor_us, "vs_floor": t_acc_us / t_floor_us,
+                   "kernels_us_p10": pct(acc_cold, 10),
                    "kernels_us_p90": pct(acc_cold, 90), "kernels_us_warm": t_acc_warm_us,
                    "kernels_us_sequential_tree": t_acc_seq_us,
                    "algorithmic_bytes_upper": work["accept_bytes"],

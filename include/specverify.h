@@ -395,6 +395,31 @@ SPEC_API int32_t spec_abi_version(void);
 SPEC_API spec_status_t spec_stream_read_probe(const void* src, size_t bytes, uint32_t* out, int32_t blocks,
                                               void* stream);
 
+/* Diagnostics: a floor for the acceptance kernels (spec_accept), reported
+ * beside their time.  Two kernels with the acceptance's memory traffic and
+ * its chain of dependent round trips (Eq. (1)'s tests need the rows'
+ * normalisers, the residual or extra-token sample of Sec. 2.2 and Sec. 4.3
+ * needs every chunk's mass, then the chosen chunk's entries) and none of its
+ * arithmetic: the first reads every entry of `num_rows` rows of V entries
+ * (elem_bytes 4 or 2, row stride `row_stride` elements) once in 4096-entry
+ * chunks of whole 16-byte units (a row's last bytes past its last whole unit
+ * are not read); the second, per request (B <= num_rows, request i owning rows
+ * [i r, (i + 1) r), r = num_rows / B) and chunk, loads a word of the
+ * first's output, a word chosen by it, a chunk of a row chosen by that,
+ * publishes a value and takes a ticket, and the request's last work-group
+ * loads the published values and a chunk chosen by them, and writes one
+ * word to `out` [B] (device memory; the words only keep the loads live).
+ * `rows` (device memory, 16-byte aligned, row stride a multiple of 16 bytes)
+ * is only read; `ws` is device memory of spec_accept_floor_probe_bytes()
+ * bytes, needing no initialisation.  Enqueued on `stream`; the caller times
+ * it.
+ * SPEC_ERR_INVALID_ARG for a null or misaligned pointer or a bad size,
+ * SPEC_ERR_WORKSPACE for a short workspace. */
+SPEC_API size_t spec_accept_floor_probe_bytes(int32_t V, int32_t num_rows, int32_t B);
+SPEC_API spec_status_t spec_accept_floor_probe(const void* rows, int64_t row_stride, int32_t elem_bytes, int32_t V,
+                                               int32_t num_rows, int32_t B, void* ws, size_t ws_bytes, uint32_t* out,
+                                               void* stream);
+
 #ifdef __cplusplus
 }
 #endif

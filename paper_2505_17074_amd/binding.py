@@ -21,7 +21,8 @@ SPEC_NOALLOC_SCRATCH_BYTES = 32 << 20
 SPEC_NOALLOC_STAGING_BYTES = 1 << 20
 
 EXPORTS = ("spec_workspace_bytes", "spec_verify_attn", "spec_accept", "spec_verify",
-           "spec_status_str", "spec_abi_version", "spec_stream_read_probe", "spec_verify_noalloc",
+           "spec_status_str", "spec_abi_version", "spec_stream_read_probe", "spec_accept_floor_probe",
+           "spec_accept_floor_probe_bytes", "spec_verify_noalloc",
            "spec_lm_head_accept", "spec_lm_head_workspace_bytes",
            "spec_sched_create", "spec_sched_destroy", "spec_sched_submit", "spec_sched_next",
            "spec_sched_report", "spec_sched_query", "spec_sched_simulate")
@@ -187,6 +188,11 @@ def load(path: str = LIB_PATH) -> C.CDLL:
     lib.spec_abi_version.restype = C.c_int32
     lib.spec_stream_read_probe.argtypes = [C.c_void_p, C.c_size_t, C.c_void_p, C.c_int32, C.c_void_p]
     lib.spec_stream_read_probe.restype = C.c_int
+    lib.spec_accept_floor_probe_bytes.argtypes = [C.c_int32, C.c_int32, C.c_int32]
+    lib.spec_accept_floor_probe_bytes.restype = C.c_size_t
+    lib.spec_accept_floor_probe.argtypes = [C.c_void_p, C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                            C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p]
+    lib.spec_accept_floor_probe.restype = C.c_int
     lib.spec_sched_create.argtypes = [C.c_int32, P(SpecSchedParams), C.c_int32, P(C.c_void_p)]
     lib.spec_sched_create.restype = C.c_int
     lib.spec_sched_destroy.argtypes = [C.c_void_p]
@@ -260,6 +266,14 @@ def spec_abi_version() -> int:
 
 def spec_stream_read_probe(src, nbytes, out, blocks, stream):
     return load().spec_stream_read_probe(src, nbytes, out, blocks, stream)
+
+
+def spec_accept_floor_probe_bytes(V, num_rows, B):
+    return int(load().spec_accept_floor_probe_bytes(V, num_rows, B))
+
+
+def spec_accept_floor_probe(rows, row_stride, elem_bytes, V, num_rows, B, ws, ws_bytes, out, stream):
+    return load().spec_accept_floor_probe(rows, row_stride, elem_bytes, V, num_rows, B, ws, ws_bytes, out, stream)
 
 
 def make_requests(ctx_len, draft_len=None, tree_parent=None, tree_parents=None):

@@ -924,4 +924,40 @@ spec_status_t spec_stream_read_probe(const void* src, size_t bytes, uint32_t* ou
              : SPEC_ERR_HIP;
 }
 
+// The floor probe's workspace: the stream's words [num_rows, chunks], the
+// tickets [B], the published values [B, chunks].
+static size_t floor_layout(int32_t V, int32_t num_rows, int32_t B, size_t* off_tickets, size_t* off_sums) {
+  const int64_t nch = ((int64_t)V + 4095) / 4096;
+  size_t off = align_up(sizeof(uint32_t) * (size_t)((int64_t)num_rows * nch));
+  *off_tickets = off;
+  off = align_up(off + sizeof(int32_t) * (size_t)B);
+  *off_sums = off;
+  return align_up(off + sizeof(uint64_t) * (size_t)((int64_t)B * nch));
+}
+
+size_t spec_accept_floor_probe_bytes(int32_t V, int32_t num_rows, int32_t B) {
+  if (V < 1 || B < 1 || num_rows < B) return 0;
+  size_t a, b;
+  return floor_layout(V, num_rows, B, &a, &b);
+}
+
+spec_status_t spec_accept_floor_probe(const void* rows, int64_t row_stride, int32_t elem_bytes, int32_t V,
+                                      int32_t num_rows, int32_t B, void* ws, size_t ws_bytes, uint32_t* out,
+                                      void* stream) {
+  if (!rows || !ws || !out || !aligned16(rows) || !aligned16(ws) || (elem_bytes != 2 && elem_bytes != 4) || V < 1 ||
+      B < 1 || num_rows < B || row_stride < V || (row_stride * elem_bytes) % 16 != 0)
+    return SPEC_ERR_INVALID_ARG;
+  const int64_t nch = ((int64_t)V + 4095) / 4096;
+  if ((int64_t)num_rows * nch > INT32_MAX) return SPEC_ERR_INVALID_ARG;
+  size_t ot, os;
+  if (ws_bytes < floor_layout(V, num_rows, B, &ot, &os)) return SPEC_ERR_WORKSPACE;
+  char* w = static_cast<char*>(ws);
+  return sv::launch_accept_floor(rows, row_stride * elem_bytes, (int64_t)V * elem_bytes, 4096 * (int64_t)elem_bytes,
+                                 (int)nch, num_rows, B, reinterpret_cast<uint32_t*>(w),
+                                 reinterpret_cast<int32_t*>(w + ot), reinterpret_cast<uint64_t*>(w + os), out,
+                                 static_cast<hipStream_t>(stream)) == hipSuccess
+             ? SPEC_OK
+             : SPEC_ERR_HIP;
+}
+
 }  // extern "C"

@@ -134,6 +134,11 @@ hipError_t launch_decide(const AccParams& p, hipStream_t s);
 // and 4 (draft probability at a draft token not > 0).
 hipError_t launch_accept_validate(const AccParams& p, uint32_t* flag, hipStream_t s);
 hipError_t launch_stream_read(const void* src, size_t bytes, uint32_t* out, int blocks, hipStream_t s);
+// The acceptance floor probe's two kernels (stream, then the chain of
+// dependent round trips) over num_rows (>= B) rows of v_bytes each.
+hipError_t launch_accept_floor(const void* rows, int64_t row_bytes, int64_t v_bytes, int64_t chunk_bytes, int nch,
+                               int num_rows, int B, uint32_t* sink, int32_t* tickets, uint64_t* sums, uint32_t* out,
+                               hipStream_t s);
 
 // The no-allocation entry point's device scratch (a static device array of
 // kNoAllocScratchBytes) and its host staging (a static host array of

@@ -207,6 +207,32 @@ def test_stream_probe_rejects_bad_arguments(lib):
     assert B.spec_stream_read_probe(FAKE, 1024, FAKE, 65537, None) == B.SPEC_ERR_INVALID_ARG
 
 
+def test_accept_floor_probe_rejects_bad_arguments(lib):
+    # sizes: stream output per (row, chunk), tickets, published values, outputs
+    n = B.spec_accept_floor_probe_bytes(32000, 716, 128)
+    assert n >= 4 * 716 * 8 + 4 * 128 + 8 * 128 * 8
+    assert B.spec_accept_floor_probe_bytes(32000, 100, 128) == 0      # fewer rows than requests
+    assert B.spec_accept_floor_probe_bytes(0, 716, 128) == 0
+    # every case fails its host check before any HIP call
+    ok = (FAKE, 32000, 4, 32000, 716, 128, FAKE, n, FAKE, None)
+    def call(**kw):
+        args = list(ok)
+        for i, k in enumerate(("rows", "stride", "eb", "V", "num_rows", "B", "ws", "ws_bytes", "out", "stream")):
+            if k in kw:
+                args[i] = kw[k]
+        return B.spec_accept_floor_probe(*args)
+    assert call(rows=0) == B.SPEC_ERR_INVALID_ARG
+    assert call(rows=FAKE + 8) == B.SPEC_ERR_INVALID_ARG
+    assert call(ws=0) == B.SPEC_ERR_INVALID_ARG
+    assert call(out=0) == B.SPEC_ERR_INVALID_ARG
+    assert call(eb=3) == B.SPEC_ERR_INVALID_ARG
+    assert call(stride=31999) == B.SPEC_ERR_INVALID_ARG             # shorter than a row
+    assert call(stride=32002, eb=2) == B.SPEC_ERR_INVALID_ARG       # rows not 16-byte aligned
+    assert call(num_rows=127) == B.SPEC_ERR_INVALID_ARG
+    assert call(V=0) == B.SPEC_ERR_INVALID_ARG
+    assert call(ws_bytes=n - 1) == B.SPEC_ERR_WORKSPACE
+
+
 def test_struct_layouts_match_the_header(tmp_path):
     """The ctypes structures of the binding against the C header, field by
     field (offsets and sizes from a program compiled with the system gcc)."""

@@ -109,3 +109,52 @@ def test_stream_read_probe_reads_every_word(gpu_lib):
         got = np.bitwise_xor.reduce(out[:blocks].cpu().numpy().view(np.uint32))
         want = np.bitwise_xor.reduce(src.cpu().numpy().view(np.uint32))
         assert got == want, blocks
+
+
+def _floor_emulated(rows_u8, eb, V, num_rows, B_):
+    """The acceptance floor probe's output words, step by step on the host."""
+    nch = (V + 4095) // 4096
+
+    def chunk_xor(r, c):
+        c0 = c * 4096 * eb
+        c1 = min(c0 + 4096 * eb, V * eb)
+        n16 = (c1 - c0) // 16
+        w = rows_u8[r, c0:c0 + 16 * n16].view(np.uint32)
+        return int(np.bitwise_xor.reduce(w)) if w.size else 0
+
+    sink = np.array([[chunk_xor(r, c) for c in range(nch)] for r in range(num_rows)], np.uint64)
+    rpr = num_rows // B_
+    out = np.zeros(B_, np.uint32)
+    for i in range(B_):
+        r0 = i * rpr
+        x = 0
+        for c in range(nch):
+            a = int(sink[r0, c])
+            b = int(sink[r0 + a % rpr, c])
+            x ^= chunk_xor(r0 + b % rpr, c) | 1
+        pick = x % nch
+        out[i] = chunk_xor(r0 + pick % rpr, pick)
+    return out
+
+
+@pytest.mark.parametrize("eb,V,stride,num_rows,B_", [
+    (4, 32000, 32000, 40, 8),       # the LLaMA vocabulary, fp32
+    (2, 128256, 128256, 18, 6),     # the long-context vocabulary, bf16
+    (4, 5000, 5120, 9, 4),          # a ragged last chunk, padded rows, a row no request owns
+])
+def test_accept_floor_probe_reads_what_it_claims(gpu_lib, eb, V, stride, num_rows, B_):
+    print(f"[case] acceptance floor probe eb {eb} V {V} rows {num_rows} B {B_}", flush=True)
+    g = torch.Generator().manual_seed(V + num_rows)
+    words = stride * eb // 4
+    host = torch.randint(0, 1 << 31, (num_rows, words), dtype=torch.int64, generator=g).to(torch.int32)
+    rows = host.to("cuda")
+    n = B.spec_accept_floor_probe_bytes(V, num_rows, B_)
+    ws = torch.randint(0, 256, (n,), dtype=torch.uint8, device="cuda")       # junk: no initialisation needed
+    out = torch.zeros(B_, dtype=torch.int32, device="cuda")
+    want = _floor_emulated(host.numpy().view(np.uint8).reshape(num_rows, -1), eb, V, num_rows, B_)
+    for _ in range(2):                                                       # the tickets start over each call
+        out.fill_(0)
+        B.check(B.spec_accept_floor_probe(rows.data_ptr(), stride, eb, V, num_rows, B_, ws.data_ptr(), n,
+                                          out.data_ptr(), torch.cuda.current_stream().cuda_stream), "floor probe")
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy().view(np.uint32), want)
