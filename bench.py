@@ -260,8 +260,8 @@ def lm_head_figures(name: str, seed: int, dev, flush, reps: int = 10) -> dict:
     workload's verify positions: the GEMM's time (events around its kernel,
     after a cache flush), its MFMA and HBM rooflines, torch's bf16 linear
     (hipBLASLt) on the same tensors as a reference point, and the fused
-    acceptance (statistics fold + decision) beside the unfused one (row pass
-    + decision) on the same logits."""
+    acceptance (the decision on the GEMM's tile statistics) beside the
+    unfused one (row pass + decision) on the same logits."""
     import numpy as np
     import torch
     from paper_2505_17074_amd import binding as B

@@ -390,15 +390,17 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
     }
   }
 
-  // (M, Z) of every row of the request that has chunk statistics
+  // (M, Z) of every row of the request that has chunk statistics (after the
+  // LM head, its tile statistics: the same fold over 16 times as many entries)
+  const int nst = p.tiles ? p.ntiles : p.nch;
   for (int r = wv; r < N; r += kAccThreads / 64) {
     if (p.tree == 1 && !p.all_stats && p.topo.qrank[r] < 0) continue;     // a leaf's row: none yet
-    const ChunkStat* st = p.rowstats + (int64_t)(rq.q0 + r) * p.nch;
+    const ChunkStat* st = (p.tiles ? p.tiles : p.rowstats) + (int64_t)(rq.q0 + r) * nst;
     float m = -INFINITY;
-    for (int k = ln; k < p.nch; k += 64) m = fmaxf(m, st[k].m);
+    for (int k = ln; k < nst; k += 64) m = fmaxf(m, st[k].m);
     for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
     double z = 0.0;
-    for (int k = ln; k < p.nch; k += 64) z += st[k].s * exp((double)st[k].m - (double)m);
+    for (int k = ln; k < nst; k += 64) z += st[k].s * exp((double)st[k].m - (double)m);
     for (int o = 32; o >= 1; o >>= 1) z += __shfl_xor(z, o);
     if (ln == 0) {
       s_M[r] = m;
@@ -513,10 +515,24 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   if (!residual) {
     // the chosen row's chunk statistics (device-scope loads: a leaf's were
     // written by this kernel's work-groups), masses in units of exp(M)
-    for (int k = tid; k < p.nch; k += kAccThreads) {
-      s_mass[k] = load_dev(&rst[k].s);
-      s_mc[k] = __uint_as_float(__hip_atomic_load(reinterpret_cast<const uint32_t*>(&rst[k].m), __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT));
+    if (p.tiles) {
+      // after the LM head: each chunk's statistics folded from its tiles
+      const ChunkStat* ts = p.tiles + (int64_t)d.row * p.ntiles;
+      for (int k = tid; k < p.nch; k += kAccThreads) {
+        const int t0 = k * kLmhTilesPerChunk, t1 = min(t0 + kLmhTilesPerChunk, p.ntiles);
+        float m = -INFINITY;
+        for (int t = t0; t < t1; ++t) m = fmaxf(m, ts[t].m);
+        double sum = 0.0;
+        for (int t = t0; t < t1; ++t) sum += ts[t].s * exp((double)ts[t].m - (double)m);
+        s_mass[k] = sum;
+        s_mc[k] = m;
+      }
+    } else {
+      for (int k = tid; k < p.nch; k += kAccThreads) {
+        s_mass[k] = load_dev(&rst[k].s);
+        s_mc[k] = __uint_as_float(__hip_atomic_load(reinterpret_cast<const uint32_t*>(&rst[k].m), __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT));
+      }
     }
     __syncthreads();
     if (tid == 0) {

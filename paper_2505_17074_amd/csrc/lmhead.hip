@@ -109,6 +109,15 @@ __global__ __launch_bounds__(kLmhThreads) __attribute__((amdgpu_waves_per_eu(kLm
   // tile are 8 blocks apart (one XCD of the round-robin dispatch) and within
   // one window of 8 * m_tiles blocks, so they run together and share that
   // tile's weight rows in the XCD's L2
+  // the decision kernel's inputs the row-statistics kernel would otherwise
+  // prepare (every work-group may take part; the grid can be smaller than B)
+  for (int b = blockIdx.x; b < p.B; b += gridDim.x) {
+    if (threadIdx.x < 2)
+      reinterpret_cast<uint4*>(p.reqs + b)[threadIdx.x] = reinterpret_cast<const uint4*>(p.reqs_src + b)[threadIdx.x];
+    if (threadIdx.x == 0) p.tickets[b] = 0;
+  }
+  for (int x = blockIdx.x * kLmhThreads + threadIdx.x; x < p.nodes_n16; x += gridDim.x * kLmhThreads)
+    reinterpret_cast<uint4*>(p.nodes)[x] = reinterpret_cast<const uint4*>(p.nodes_src)[x];
   const int T = p.m_tiles;
   const int g = blockIdx.x / (8 * T), r8 = blockIdx.x % (8 * T);
   const int mt = r8 / 8, nt = g * 8 + (r8 % 8);

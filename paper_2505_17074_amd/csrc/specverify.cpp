@@ -751,8 +751,8 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
   }
 
   if (mode.lm) {
-    // the LM head, then its tile statistics folded into chunk statistics,
-    // then the decision and final sample, all on the caller's stream
+    // the LM head, then the decision and final sample (folding the head's
+    // tile statistics), all on the caller's stream
     const spec_lm_head_args_t* lm = mode.lm;
     sv::LmhParams g{};
     g.hidden = static_cast<const uint16_t*>(lm->hidden);
@@ -771,11 +771,26 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     g.tile_rows = geo.tile_rows;
     g.m_tiles = geo.m_tiles;
     g.out_bf16 = acc->dtype == SPEC_BF16;
+    // The decision kernel folds the tile statistics itself, and the GEMM does
+    // the row-statistics kernel's other duties; the sequential sibling rule
+    // reads chunk statistics, which the fold kernel writes.
+    const bool fold = c.tree == 2;
+    if (!fold) {
+      c.tiles = g.tiles;
+      c.ntiles = g.ntiles;
+      g.reqs_src = c.reqs_src;
+      g.reqs = c.reqs;
+      g.tickets = c.tickets;
+      g.nodes_src = c.nodes_src;
+      g.nodes = c.nodes;
+      g.nodes_n16 = c.per_req ? c.nodes_n16 : 0;
+      g.B = c.B;
+    }
     if (lm->event_begin && hipEventRecord(static_cast<hipEvent_t>(lm->event_begin), s) != hipSuccess) return SPEC_ERR_HIP;
     if (sv::launch_lmh(g, s) != hipSuccess) return SPEC_ERR_HIP;
     if (lm->event_end && hipEventRecord(static_cast<hipEvent_t>(lm->event_end), s) != hipSuccess) return SPEC_ERR_HIP;
     if (acc->event_begin && hipEventRecord(static_cast<hipEvent_t>(acc->event_begin), s) != hipSuccess) return SPEC_ERR_HIP;
-    if (sv::launch_foldstats(c, g.tiles, g.ntiles, s) != hipSuccess) return SPEC_ERR_HIP;
+    if (fold && sv::launch_foldstats(c, g.tiles, g.ntiles, s) != hipSuccess) return SPEC_ERR_HIP;
     if (acc->event_mid && hipEventRecord(static_cast<hipEvent_t>(acc->event_mid), s) != hipSuccess) return SPEC_ERR_HIP;
     if (sv::launch_decide(c, s) != hipSuccess) return SPEC_ERR_HIP;
     if (acc->event_end && hipEventRecord(static_cast<hipEvent_t>(acc->event_end), s) != hipSuccess) return SPEC_ERR_HIP;

@@ -79,6 +79,11 @@ struct AccParams {
   // slots [B, kMaxNodes, seq_groups]
   int32_t seq_groups;
   SeqSlot* seq_slots;
+  // after the LM head (tiles != nullptr): the decision kernel folds the GEMM's
+  // per-(row, kLmhNT-entry tile) statistics itself [Nq, ntiles], and rowstats
+  // is not written
+  const ChunkStat* tiles;
+  int32_t ntiles;
 };
 
 constexpr int kAccMaxChunks = 1024;    // vocabularies up to 4M entries
@@ -99,6 +104,16 @@ struct LmhParams {
   int32_t tile_rows;        // <= the kernel's tile height 64 rb
   int32_t rb;               // 16-row blocks per wave: tile height 64 rb
   int32_t out_bf16;
+  // the row-statistics kernel's other duties for the decision kernel that
+  // follows: the request table's device copy (and the node table's, per-request
+  // trees) and cleared tickets, done by the first work-groups
+  const ReqInfo* reqs_src;
+  ReqInfo* reqs;
+  int32_t* tickets;
+  const NodeInfo* nodes_src;
+  NodeInfo* nodes;
+  int32_t nodes_n16;
+  int32_t B;
 };
 struct LmhGeometry {
   int32_t rb, tile_rows, m_tiles;
