@@ -392,15 +392,38 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
 
   // (M, Z) of every row of the request that has chunk statistics (after the
   // LM head, its tile statistics: the same fold over 16 times as many entries)
+  // A row of at most 64 * kHeld statistics is loaded whole into registers
+  // before any is used (one round trip); longer rows take two passes.
+  constexpr int kHeld = 8;
   const int nst = p.tiles ? p.ntiles : p.nch;
   for (int r = wv; r < N; r += kAccThreads / 64) {
     if (p.tree == 1 && !p.all_stats && p.topo.qrank[r] < 0) continue;     // a leaf's row: none yet
     const ChunkStat* st = (p.tiles ? p.tiles : p.rowstats) + (int64_t)(rq.q0 + r) * nst;
     float m = -INFINITY;
-    for (int k = ln; k < nst; k += 64) m = fmaxf(m, st[k].m);
-    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
     double z = 0.0;
-    for (int k = ln; k < nst; k += 64) z += st[k].s * exp((double)st[k].m - (double)m);
+    if (nst <= 64 * kHeld) {
+      float hm[kHeld];
+      double hs[kHeld];
+#pragma unroll
+      for (int j = 0; j < kHeld; ++j) {
+        hm[j] = -INFINITY;
+        hs[j] = 0.0;
+        if (ln + 64 * j < nst) {
+          hm[j] = st[ln + 64 * j].m;
+          hs[j] = st[ln + 64 * j].s;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kHeld; ++j) m = fmaxf(m, hm[j]);
+      for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+#pragma unroll
+      for (int j = 0; j < kHeld; ++j)
+        if (ln + 64 * j < nst) z += hs[j] * exp((double)hm[j] - (double)m);
+    } else {
+      for (int k = ln; k < nst; k += 64) m = fmaxf(m, st[k].m);
+      for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+      for (int k = ln; k < nst; k += 64) z += st[k].s * exp((double)st[k].m - (double)m);
+    }
     for (int o = 32; o >= 1; o >>= 1) z += __shfl_xor(z, o);
     if (ln == 0) {
       s_M[r] = m;
@@ -516,16 +539,39 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
     // the chosen row's chunk statistics (device-scope loads: a leaf's were
     // written by this kernel's work-groups), masses in units of exp(M)
     if (p.tiles) {
-      // after the LM head: each chunk's statistics folded from its tiles
+      // after the LM head: each chunk's statistics folded from its tiles,
+      // one tile per thread and a chunk's tiles on consecutive lanes; kQ
+      // tiles per thread are loaded before any is used
+      static_assert(kLmhTilesPerChunk <= 64 && (kLmhTilesPerChunk & (kLmhTilesPerChunk - 1)) == 0,
+                    "a chunk's tiles fold inside one wave");
+      constexpr int kQ = 4;
       const ChunkStat* ts = p.tiles + (int64_t)d.row * p.ntiles;
-      for (int k = tid; k < p.nch; k += kAccThreads) {
-        const int t0 = k * kLmhTilesPerChunk, t1 = min(t0 + kLmhTilesPerChunk, p.ntiles);
-        float m = -INFINITY;
-        for (int t = t0; t < t1; ++t) m = fmaxf(m, ts[t].m);
-        double sum = 0.0;
-        for (int t = t0; t < t1; ++t) sum += ts[t].s * exp((double)ts[t].m - (double)m);
-        s_mass[k] = sum;
-        s_mc[k] = m;
+      for (int j0 = 0; j0 < p.ntiles; j0 += kQ * kAccThreads) {
+        float tm[kQ];
+        double tsm[kQ];
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) {
+          const int j = j0 + q * kAccThreads + tid;
+          tm[q] = -INFINITY;
+          tsm[q] = 0.0;
+          if (j < p.ntiles) {
+            tm[q] = ts[j].m;
+            tsm[q] = ts[j].s;
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < kQ; ++q) {
+          const int j = j0 + q * kAccThreads + tid;
+          float m = tm[q];
+          for (int o = kLmhTilesPerChunk / 2; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+          double sum = j < p.ntiles ? tsm[q] * exp((double)tm[q] - (double)m) : 0.0;
+          for (int o = kLmhTilesPerChunk / 2; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+          const int k = j / kLmhTilesPerChunk;
+          if (j % kLmhTilesPerChunk == 0 && k < p.nch) {
+            s_mass[k] = sum;
+            s_mc[k] = m;
+          }
+        }
       }
     } else {
       for (int k = tid; k < p.nch; k += kAccThreads) {
