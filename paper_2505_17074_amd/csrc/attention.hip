@@ -9,6 +9,7 @@
 #include "sv_attn.h"
 
 #include <algorithm>
+#include <climits>
 #include <type_traits>
 
 namespace sv {
@@ -404,6 +405,41 @@ __device__ __forceinline__ bool arrive_last(unsigned long long* ctr, uint32_t ta
   return false;
 }
 
+// Work-group 0 starts this call's count on the claim word at `base` as soon
+// as the kernel starts (unless a claim has started it already): claims begin
+// only once a first-round work-group has finished, so each is then a single
+// fetch-and-add.  (When many work-groups claim at once on a word that still
+// holds another call's value, every one of them falls back to the exchange
+// loop below, and a burst of k claims costs about k^2 exchanges.)
+__device__ __forceinline__ void claim_start(unsigned long long* ctr, uint32_t tag, int base, int bound) {
+  unsigned long long old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (int tries = 0; tries <= bound + 1 && (uint32_t)(old >> 32) != tag; ++tries)
+    if (__hip_atomic_compare_exchange_strong(ctr, &old, ((unsigned long long)tag << 32) | (uint32_t)base,
+                                             __ATOMIC_RELAXED, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+      break;
+}
+
+// The next unclaimed item (work-groups at or above p.first_round): one
+// fetch-and-add on the claim word ((call tag << 32) | next item).  A word
+// still holding another call's value (or anything else) was only bumped by
+// it; the exchange loop then starts this call's count at `base`, or takes
+// the next item if another work-group has started it meanwhile.  Every
+// failed exchange means another work-group's succeeded in between, so the
+// loop ends after at most `bound` tries; the bound only guards that.
+__device__ __forceinline__ int claim_item(unsigned long long* ctr, uint32_t tag, int base, int bound) {
+  unsigned long long old = __hip_atomic_fetch_add(ctr, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if ((uint32_t)(old >> 32) == tag) return (int)(uint32_t)old;
+  old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  for (int tries = 0; tries <= bound + 1; ++tries) {
+    const unsigned long long nw =
+        ((uint32_t)(old >> 32) == tag) ? old + 1 : (((unsigned long long)tag << 32) | (uint32_t)(base + 1));
+    if (__hip_atomic_compare_exchange_strong(ctr, &old, nw, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT))
+      return (int)((uint32_t)nw - 1u);
+  }
+  return INT_MAX;
+}
+
 // The split combine of one stream (rows = heads x verify positions of one
 // request, KV head and head group), by the work-group of its last piece:
 //   O = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s,  M = max_s m_s,
@@ -495,8 +531,18 @@ void attn_split_mfma(AttnParams p) {
 #ifdef SV_ATTN_TRACE
   unsigned long long tr_start = wall_clock64(), tr_first = 0, tr_done = 0;
 #endif
-  const AttnItem it = p.items[blockIdx.x];
+  int idx = blockIdx.x;
+  if (idx == 0 && p.first_round < (int)gridDim.x && threadIdx.x == 0)
+    claim_start(p.claim, p.call_tag, p.first_round, (int)gridDim.x);
+  if (idx >= p.first_round) {
+    __shared__ int s_item;
+    if (threadIdx.x == 0) s_item = claim_item(p.claim, p.call_tag, p.first_round, (int)gridDim.x);
+    __syncthreads();
+    idx = __builtin_amdgcn_readfirstlane(s_item);
+  }
   mirror_plan(p);
+  if (idx >= p.n_items) return;       // uniform: every item is taken
+  const AttnItem it = p.items[idx];
   const int n = it.nq;
   const int R = it.nheads * n;
   const int ctx = it.ctx;
@@ -906,7 +952,7 @@ __global__ __launch_bounds__(256) void attn_combine(AttnParams p) {
 
 template <int D, bool PG>
 hipError_t launch_mfma(const AttnParams& p, int nr, hipStream_t s) {
-  const dim3 grid(p.n_items);
+  const dim3 grid(p.grid);
   switch (nr) {
     case 1: attn_split_mfma<D, 1, SV_NS_W1, PG><<<grid, dim3(64), 0, s>>>(p); break;
     case 2: attn_split_mfma<D, 2, SV_NS_W2, PG><<<grid, dim3(128), 0, s>>>(p); break;

@@ -45,6 +45,8 @@ struct Plan {
   int split = 0;
   int64_t split_streams = 0;   // (request, KV head, head group) streams cut into pieces
   bool fused = false;          // the split kernel combines its own partials
+  int64_t grid = 0;            // work-groups of the split kernel
+  int64_t first_round = 0;     // work-groups that take their own index's item
   // acceptance
   bool has_acc = false;
   int nch = 0;
@@ -52,6 +54,7 @@ struct Plan {
   size_t off_reqs = 0, off_rowreq = 0, off_items = 0, off_nodes = 0, plan_bytes = 0;
   size_t off_acc_reqs = 0, off_acc_nodes = 0, off_tickets = 0, off_seq = 0;
   size_t off_part_o = 0, off_part_ml = 0, off_rowstats = 0, off_masses = 0, off_flag = 0, off_counters = 0;
+  size_t off_claim = 0;
   size_t device_bytes = 0;
 };
 
@@ -190,16 +193,19 @@ int piece_len(int L, int64_t s) {
 // remain a few percent of the K/V bytes a piece streams (32 rows x d x 2 x 2
 // per 32 keys), and >= 256 keys.
 //  - At least as many streams as slots: pieces of at most kMaxPiece keys,
-//    dispatched longest first.  A longer item, started first, still outlasts
-//    the rest of the kernel once the other work-groups have drained (measured
-//    on ragged batches: 6464-key pieces 28% slower than 4096).
+//    dispatched longest first, the items past the first round claimed at run
+//    time.  A work-group streams about 30 keys per microsecond, so a
+//    4096-key piece started first runs nearly as long as the whole kernel on
+//    a 128-request ragged batch (3200 keys per slot on average).  Measured
+//    there with claims, attention alone: 2048-key pieces 158 us, 2560 150,
+//    3072 146, 3328-3840 142-143, 4096 155 (and 155 without claims).
 //  - Fewer streams than slots: the smallest split whose items all fit one
 //    round of slots, so every work-group takes exactly one item and none waits
 //    for a second round (on 8 requests of 16K-32K keys x 8 KV heads, 504 items
 //    of <= 3264 keys: about 7% faster than 408 items of <= 4096 keys, and 24%
 //    faster than 528 items of <= 3072).
 #ifndef SV_MAX_PIECE
-#define SV_MAX_PIECE 4096
+#define SV_MAX_PIECE 3584
 #endif
 constexpr int64_t kMaxPiece = SV_MAX_PIECE;
 // Largest partial block (rows x pieces x d x 4 bytes) of one split stream
@@ -220,17 +226,38 @@ int64_t fuse_max_bytes() {
   return (end && *end == 0 && v >= 0) ? (int64_t)v : kFuseMaxBytes;
 }
 constexpr int64_t kMaxSplit = 1 << 20;
+// Work-groups launched beyond the item count when items are claimed at run
+// time.  Work-group b runs on XCD b % 8, and the XCDs stream at different
+// rates (the slowest 5-10 % below the fastest on ragged batches, the same
+// XCDs on every device measured), so an XCD that drains its items sooner
+// can use more work-groups than an eighth of the items; the surplus finds
+// nothing left and ends at once.  Measured on the 128-request ragged batch,
+// 0 to 384 surplus work-groups are within 0.5 us of each other: the claims'
+// gain is their order (the next item to whichever slot frees first, across
+// the XCDs), not the surplus.  The environment variable SPEC_ATTN_EXTRA_WG
+// overrides the count.
+int64_t env_count(const char* name, int64_t dflt, int64_t lo) {
+  const char* e = std::getenv(name);
+  if (!e || !*e) return dflt;
+  char* end = nullptr;
+  const long long v = std::strtoll(e, &end, 10);
+  return (end && *end == 0 && v >= lo && v <= (1 << 20)) ? (int64_t)v : dflt;
+}
+// Work-groups that take their own index's item: one round of slots.  The
+// environment variable SPEC_ATTN_FIRST_ROUND overrides it (tests use it to
+// reach the claims with few items).
+int64_t claim_first_round(int64_t slots) { return env_count("SPEC_ATTN_FIRST_ROUND", slots, 1); }
+int64_t claim_extra(int64_t n_items) {
+  return env_count("SPEC_ATTN_EXTRA_WG", (n_items / 6 + 7) / 8 * 8, 0);
+}
 // Keys per piece of each request's streams (every KV head and head group of
 // a request has the same length).  `slots` = work-groups the device runs at
 // once; `len[i]` = keys of request i, each the length of `mult[i]` streams.
 // Pieces stay >= 40 * rows keys, so the fp32 partials (rows x d x 4 bytes,
 // written once and read once by the combine) remain a few percent of the K/V
 // bytes a piece streams (32 rows x d x 2 x 2 per 32 keys), and >= 256 keys.
-//  - At least as many streams as slots: pieces of at most kMaxPiece keys,
-//    dispatched longest first.  A longer item, started first, still outlasts
-//    the rest of the kernel once the other work-groups have drained (measured
-//    on ragged batches: 6464-key pieces 28% slower than 4096; 2048 and 3072
-//    were 4% and 2% slower than 4096).
+//  - At least as many streams as slots: pieces of at most kMaxPiece keys
+//    (above), dispatched longest first.
 //  - Fewer streams than slots: every work-group takes exactly one item (a
 //    second, nearly empty round of items ran 7-27% slower), and the pieces
 //    are cut so that the longest is as short as the slots allow: one piece
@@ -459,7 +486,16 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
       for (const AttnItem& it : P.items) sorted[start[max_t - (it.ke - it.kb + 31) / 32]++] = it;
       P.items.swap(sorted);
     }
-    if (part >= INT32_MAX) return SPEC_ERR_INVALID_ARG;
+    // Items past the first round of slots go to whichever work-groups start
+    // next (bf16 kernel; see claim_extra).
+    const int64_t n_it = (int64_t)P.items.size();
+    const int64_t first = claim_first_round(slots);
+    P.first_round = P.grid = n_it;
+    if (bf && n_it > first) {
+      P.first_round = first;
+      P.grid = n_it + claim_extra(n_it);
+    }
+    if (part >= INT32_MAX || P.grid >= INT32_MAX) return SPEC_ERR_INVALID_ARG;
     P.parts = part;
     P.nr_max = nr;
     // The bf16 kernel combines a split stream's partials itself (the last
@@ -509,6 +545,8 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   off = align_up(off + sizeof(float) * 2 * (size_t)P.parts);
   P.off_counters = off;                // the fused combine's arrival counters
   off = align_up(off + sizeof(unsigned long long) * (size_t)(P.fused ? P.split_streams : 0));
+  P.off_claim = off;                   // the split kernel's claim word
+  off = align_up(off + (P.grid > P.first_round ? sizeof(unsigned long long) : 0));
   P.off_rowstats = off;
   off = align_up(off + sizeof(sv::ChunkStat) * (size_t)(P.has_acc ? P.Nq * P.nch : 0));
   P.off_masses = off;
@@ -661,9 +699,12 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     a.items = reinterpret_cast<const AttnItem*>(pl + P.off_items);
     a.reqs = reinterpret_cast<const ReqInfo*>(d + P.off_reqs);
     a.row_req = reinterpret_cast<const int32_t*>(d + P.off_rowreq);
+    a.grid = (int32_t)P.grid;
+    a.first_round = (int32_t)P.first_round;
+    if (P.fused || P.grid > P.first_round) a.call_tag = next_call_tag();
+    if (P.grid > P.first_round) a.claim = reinterpret_cast<unsigned long long*>(d + P.off_claim);
     if (P.fused) {
       a.counters = reinterpret_cast<unsigned long long*>(d + P.off_counters);
-      a.call_tag = next_call_tag();
       a.fused = 1;
     } else if (P.parts > 0 && pl != d) {      // the combine kernel runs: mirror its table and map
       const bool mfma = attn->dtype == SPEC_BF16;

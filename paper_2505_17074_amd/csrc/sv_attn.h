@@ -74,6 +74,15 @@ struct AttnParams {
   unsigned long long* counters;
   uint32_t call_tag;
   int32_t fused;
+  // Work-groups of the bf16 split kernel (grid >= n_items).  Work-group b <
+  // first_round takes item b; every later one claims the next item from
+  // *claim ((call tag << 32) | next item; a word holding another tag starts
+  // over at first_round) and leaves when none is left.  Later work-groups are
+  // dispatched as earlier ones end, so the XCDs that drain their items sooner
+  // take more of the rest.  first_round = grid = n_items: no claims.
+  int32_t grid;
+  int32_t first_round;
+  unsigned long long* claim;
 };
 
 // Largest number of query rows (heads x verify positions) one work item holds.

@@ -351,6 +351,30 @@ def test_per_request_trees_size_like_the_shared_tree(lib):
     assert per[2] >= shared[2] + 8 * 21 and per[1] >= shared[1] + 8 * 21
 
 
+def test_claim_word_in_the_workspace(lib, monkeypatch):
+    """When the bf16 split kernel has more items than its first round of
+    work-groups, the later work-groups claim items from one word in the
+    workspace (one more 256-byte section); the fp32 VALU kernel never claims,
+    and malformed environment values are ignored."""
+    req = _req(ctx=(3000, 5000))
+    monkeypatch.setenv("SPEC_ATTN_FIRST_ROUND", str(1 << 20))
+    static = _ws(req, _attn(split_kv=1024), None)
+    monkeypatch.setenv("SPEC_ATTN_FIRST_ROUND", "1")
+    claimed = _ws(req, _attn(split_kv=1024), None)
+    monkeypatch.setenv("SPEC_ATTN_EXTRA_WG", "100")          # more work-groups: the same workspace
+    assert _ws(req, _attn(split_kv=1024), None) == claimed
+    assert static[0] == claimed[0] == B.SPEC_OK and claimed[1] == static[1] + 256
+    f32 = dict(dtype=B.SPEC_F32)
+    assert _ws(req, _attn(split_kv=1024, **f32), None)[1] == _ws(req, _attn(split_kv=1024, **f32), None)[1]
+    monkeypatch.setenv("SPEC_ATTN_FIRST_ROUND", str(1 << 20))
+    f32_static = _ws(req, _attn(split_kv=1024, **f32), None)
+    monkeypatch.setenv("SPEC_ATTN_FIRST_ROUND", "1")
+    assert _ws(req, _attn(split_kv=1024, **f32), None) == f32_static
+    for bad in ("0", "-3", "x", "1.5"):                       # ignored: one round of slots
+        monkeypatch.setenv("SPEC_ATTN_FIRST_ROUND", bad)
+        assert _ws(req, _attn(split_kv=1024), None) == static
+
+
 def test_fused_combine_counters_in_the_workspace(lib, monkeypatch):
     """Split streams whose partial blocks are under the planner's limit are
     combined inside the bf16 split kernel, which needs one arrival counter per
