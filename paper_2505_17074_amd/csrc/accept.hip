@@ -344,7 +344,12 @@ __device__ __forceinline__ double load_dev(const double* p) {
 //   samples: prefix over the chunk masses, the chunk holding u * total, an
 //   fp64 scan inside it (for p, in that chunk's units exp(l - m_c)), the
 //   smallest token id whose cumulative weight exceeds the target.
-template <typename T>
+// TILES: the statistics are the LM head's per-tile ones (p.tiles), folded
+// here; otherwise the row-statistics kernel's chunk statistics.  A separate
+// build, so the verify path keeps the smaller register footprint (80 VGPRs
+// against 96 with the tile fold's held loads: 6 waves per SIMD instead of 5
+// beside the attention).
+template <typename T, bool TILES>
 __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   __shared__ double redd[4];
   __shared__ float redf[4];
@@ -392,16 +397,17 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
 
   // (M, Z) of every row of the request that has chunk statistics (after the
   // LM head, its tile statistics: the same fold over 16 times as many entries)
-  // A row of at most 64 * kHeld statistics is loaded whole into registers
-  // before any is used (one round trip); longer rows take two passes.
+  // A row of at most 64 * kHeld tile statistics is loaded whole into
+  // registers before any is used (one round trip); chunk statistics (at
+  // most a few per lane) and longer rows take two passes.
   constexpr int kHeld = 8;
-  const int nst = p.tiles ? p.ntiles : p.nch;
+  const int nst = TILES ? p.ntiles : p.nch;
   for (int r = wv; r < N; r += kAccThreads / 64) {
     if (p.tree == 1 && !p.all_stats && p.topo.qrank[r] < 0) continue;     // a leaf's row: none yet
-    const ChunkStat* st = (p.tiles ? p.tiles : p.rowstats) + (int64_t)(rq.q0 + r) * nst;
+    const ChunkStat* st = (TILES ? p.tiles : p.rowstats) + (int64_t)(rq.q0 + r) * nst;
     float m = -INFINITY;
     double z = 0.0;
-    if (nst <= 64 * kHeld) {
+    if (TILES && nst <= 64 * kHeld) {
       float hm[kHeld];
       double hs[kHeld];
 #pragma unroll
@@ -538,7 +544,7 @@ __global__ __launch_bounds__(kAccThreads) void acc_decide_select(AccParams p) {
   if (!residual) {
     // the chosen row's chunk statistics (device-scope loads: a leaf's were
     // written by this kernel's work-groups), masses in units of exp(M)
-    if (p.tiles) {
+    if constexpr (TILES) {
       // after the LM head: each chunk's statistics folded from its tiles,
       // one tile per thread and a chunk's tiles on consecutive lanes; kQ
       // tiles per thread are loaded before any is used
@@ -1234,8 +1240,14 @@ hipError_t launch_decide(const AccParams& p, hipStream_t s) {
     else acc_tree_seq<float><<<grid, dim3(kSeqThreads), 0, s>>>(p);
     return hipGetLastError();
   }
-  if (p.bf16) acc_decide_select<uint16_t><<<dim3(p.B * p.nch), block, 0, s>>>(p);
-  else acc_decide_select<float><<<dim3(p.B * p.nch), block, 0, s>>>(p);
+  const dim3 grid((unsigned)(p.B * p.nch));
+  if (p.tiles) {
+    if (p.bf16) acc_decide_select<uint16_t, true><<<grid, block, 0, s>>>(p);
+    else acc_decide_select<float, true><<<grid, block, 0, s>>>(p);
+  } else {
+    if (p.bf16) acc_decide_select<uint16_t, false><<<grid, block, 0, s>>>(p);
+    else acc_decide_select<float, false><<<grid, block, 0, s>>>(p);
+  }
   return hipGetLastError();
 }
 
