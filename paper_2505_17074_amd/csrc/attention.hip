@@ -9,6 +9,7 @@
 #include "sv_attn.h"
 
 #include <algorithm>
+#include <atomic>
 #include <climits>
 #include <type_traits>
 
@@ -406,11 +407,13 @@ __device__ __forceinline__ bool arrive_last(unsigned long long* ctr, uint32_t ta
 }
 
 // Work-group 0 starts this call's count on the claim word at `base` as soon
-// as the kernel starts (unless a claim has started it already): claims begin
-// only once a first-round work-group has finished, so each is then a single
-// fetch-and-add.  (When many work-groups claim at once on a word that still
-// holds another call's value, every one of them falls back to the exchange
-// loop below, and a burst of k claims costs about k^2 exchanges.)
+// as the kernel starts (unless a claim has started it already).  The first
+// round holds every work-group the device keeps resident at once, so claims
+// begin only once a first-round work-group has finished, and each is then a
+// single fetch-and-add.  (When many work-groups claim at once on a word that
+// still holds another call's value, each exchange loop below succeeds for
+// one of them at a time: a burst of k claims would cost about k^2 exchanges.
+// So a claim that meets another call's value first waits for this start.)
 __device__ __forceinline__ void claim_start(unsigned long long* ctr, uint32_t tag, int base, int bound) {
   unsigned long long old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   for (int tries = 0; tries <= bound + 1 && (uint32_t)(old >> 32) != tag; ++tries)
@@ -422,13 +425,26 @@ __device__ __forceinline__ void claim_start(unsigned long long* ctr, uint32_t ta
 // The next unclaimed item (work-groups at or above p.first_round): one
 // fetch-and-add on the claim word ((call tag << 32) | next item).  A word
 // still holding another call's value (or anything else) was only bumped by
-// it; the exchange loop then starts this call's count at `base`, or takes
-// the next item if another work-group has started it meanwhile.  Every
-// failed exchange means another work-group's succeeded in between, so the
-// loop ends after at most `bound` tries; the bound only guards that.
+// it.  The claim then polls the word (kClaimPolls reads, a short sleep
+// apart, roughly 100 us in all) for work-group 0's start of this call's count
+// and claims again once it is there; work-group 0 was dispatched first, so
+// it is running.  Should the polls run out, the exchange loop starts the
+// count at `base` itself, or takes the next item if another work-group has
+// started it meanwhile.  Every failed exchange means another work-group's
+// succeeded in between, so the loop ends after at most `bound` tries; the
+// bound only guards that.
+constexpr int kClaimPolls = 64;
 __device__ __forceinline__ int claim_item(unsigned long long* ctr, uint32_t tag, int base, int bound) {
   unsigned long long old = __hip_atomic_fetch_add(ctr, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if ((uint32_t)(old >> 32) == tag) return (int)(uint32_t)old;
+  for (int i = 0; i < kClaimPolls; ++i) {
+    __builtin_amdgcn_s_sleep(16);
+    old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((uint32_t)(old >> 32) == tag) {
+      old = __hip_atomic_fetch_add(ctr, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return (int)(uint32_t)old;          // the tag, once there, stays for the call
+    }
+  }
   old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   for (int tries = 0; tries <= bound + 1; ++tries) {
     const unsigned long long nw =
@@ -987,6 +1003,42 @@ int attn_lds_bytes(int D, int nr) {
     }
   };
   return D == 64 ? bytes(std::integral_constant<int, 64>{}) : bytes(std::integral_constant<int, 128>{});
+}
+
+int attn_resident_per_cu(int D, int nr, int paged) {
+  // per (D, waves, paged) build, asked once: the device's own placement
+  static std::atomic<int> cache[2][5][2] = {};
+  if ((D != 64 && D != 128) || nr < 1 || nr > 5) return 0;
+  std::atomic<int>& slot = cache[D == 128][nr - 1][paged ? 1 : 0];
+  int v = slot.load(std::memory_order_relaxed);
+  if (v != 0) return v > 0 ? v : 0;
+  auto ask = [](auto kern, int threads) {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, threads, 0) != hipSuccess) {
+      (void)hipGetLastError();
+      return -1;
+    }
+    return n > 0 ? n : -1;
+  };
+  auto by_build = [&](auto d, auto pg) -> int {
+    constexpr int DD = decltype(d)::value;
+    constexpr bool PP = decltype(pg)::value;
+    switch (nr) {
+      case 1: return ask(attn_split_mfma<DD, 1, SV_NS_W1, PP>, 64);
+      case 2: return ask(attn_split_mfma<DD, 2, SV_NS_W2, PP>, 128);
+      case 3: return ask(attn_split_mfma<DD, 3, SV_NS_W3, PP>, 192);
+      case 4: return ask(attn_split_mfma<DD, 4, SV_NS_W4, PP>, 256);
+      default: return ask(attn_split_mfma<DD, 5, SV_NS_W5, PP>, 320);
+    }
+  };
+  using I64 = std::integral_constant<int, 64>;
+  using I128 = std::integral_constant<int, 128>;
+  using T = std::true_type;
+  using F = std::false_type;
+  v = D == 64 ? (paged ? by_build(I64{}, T{}) : by_build(I64{}, F{}))
+              : (paged ? by_build(I128{}, T{}) : by_build(I128{}, F{}));
+  slot.store(v, std::memory_order_relaxed);
+  return v > 0 ? v : 0;
 }
 
 hipError_t launch_attention(const AttnParams& p, int dtype_bf16, int nr_max, hipStream_t s) {

@@ -47,6 +47,7 @@ struct Plan {
   bool fused = false;          // the split kernel combines its own partials
   int64_t grid = 0;            // work-groups of the split kernel
   int64_t first_round = 0;     // work-groups that take their own index's item
+  bool claim_word = false;     // the workspace holds the claim word
   // acceptance
   bool has_acc = false;
   int nch = 0;
@@ -243,9 +244,10 @@ int64_t env_count(const char* name, int64_t dflt, int64_t lo) {
   const long long v = std::strtoll(e, &end, 10);
   return (end && *end == 0 && v >= lo && v <= (1 << 20)) ? (int64_t)v : dflt;
 }
-// Work-groups that take their own index's item: one round of slots.  The
-// environment variable SPEC_ATTN_FIRST_ROUND overrides it (tests use it to
-// reach the claims with few items).
+// Work-groups that take their own index's item: by default every
+// work-group the device holds at once.  The environment variable
+// SPEC_ATTN_FIRST_ROUND overrides it (tests use it to reach the claims with
+// few items).
 int64_t claim_first_round(int64_t slots) { return env_count("SPEC_ATTN_FIRST_ROUND", slots, 1); }
 int64_t claim_extra(int64_t n_items) {
   return env_count("SPEC_ATTN_EXTRA_WG", (n_items / 6 + 7) / 8 * 8, 0);
@@ -265,9 +267,12 @@ int64_t claim_extra(int64_t n_items) {
 //    request whose pieces are currently longest, while its streams' extra
 //    items still fit the slots.  Every work-group streams at about the same
 //    rate, so the longest piece sets the kernel's end.
+#ifndef SV_MIN_PIECE_ROWS
+#define SV_MIN_PIECE_ROWS 40
+#endif
 std::vector<int> piece_lengths(const std::vector<int>& len, const std::vector<int>& mult, int rows_max, int64_t slots) {
   slots = std::max<int64_t>(slots, 1);
-  int64_t lo = std::max<int64_t>(40 * (int64_t)rows_max, 256);
+  int64_t lo = std::max<int64_t>(SV_MIN_PIECE_ROWS * (int64_t)rows_max, 256);
   lo = std::min<int64_t>((lo + 31) / 32 * 32, kMaxSplit);
   const size_t B = len.size();
   std::vector<int> out(B);
@@ -486,11 +491,17 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
       for (const AttnItem& it : P.items) sorted[start[max_t - (it.ke - it.kb + 31) / 32]++] = it;
       P.items.swap(sorted);
     }
-    // Items past the first round of slots go to whichever work-groups start
-    // next (bf16 kernel; see claim_extra).
+    // Items past the first round go to whichever work-groups start next
+    // (bf16 kernel; see claim_extra).  The first round is every work-group
+    // the device holds at once (at least the plan's slots), so no claim
+    // starts before a first-round work-group has ended.  The workspace keeps
+    // the claim word whenever there are more items than slots, whatever the
+    // device reports.
     const int64_t n_it = (int64_t)P.items.size();
-    const int64_t first = claim_first_round(slots);
+    const int64_t resident = (int64_t)device_cus() * sv::attn_resident_per_cu(D, nr, attn->block_table != nullptr);
+    const int64_t first = claim_first_round(std::max(slots, resident));
     P.first_round = P.grid = n_it;
+    P.claim_word = bf && n_it > std::min(first, slots);
     if (bf && n_it > first) {
       P.first_round = first;
       P.grid = n_it + claim_extra(n_it);
@@ -546,7 +557,7 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
   P.off_counters = off;                // the fused combine's arrival counters
   off = align_up(off + sizeof(unsigned long long) * (size_t)(P.fused ? P.split_streams : 0));
   P.off_claim = off;                   // the split kernel's claim word
-  off = align_up(off + (P.grid > P.first_round ? sizeof(unsigned long long) : 0));
+  off = align_up(off + (P.claim_word ? sizeof(unsigned long long) : 0));
   P.off_rowstats = off;
   off = align_up(off + sizeof(sv::ChunkStat) * (size_t)(P.has_acc ? P.Nq * P.nch : 0));
   P.off_masses = off;

@@ -89,6 +89,10 @@ struct AttnParams {
 int max_rows_per_item(int dtype_bf16, int D);
 
 hipError_t launch_attention(const AttnParams& p, int dtype_bf16, int nr_max, hipStream_t s);
+// Work-groups of the bf16 split kernel's build for head dim D, nr waves and
+// the paged or packed layout that one compute unit holds at once, as the
+// device reports it; 0 where it cannot be asked (no device).
+int attn_resident_per_cu(int D, int nr, int paged);
 // LDS bytes of the bf16 split kernel's build for head dim D and nr row tiles
 // (the fused combine stages its weights there).
 int attn_lds_bytes(int D, int nr);
