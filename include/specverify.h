@@ -54,8 +54,16 @@
  *     the arguments is read.
  *   - The device workspace needs no initialisation and may hold anything
  *     between calls: every byte a call reads is written earlier in the same
- *     call, except the split-KV arrival counters, which carry a tag that is
- *     new on every call and start over when it does not match.
+ *     call, except the split-KV arrival counters and the attention's item
+ *     claim word, which carry a tag that is new on every call and start over
+ *     when it does not match.
+ *   - When the bf16 verify attention has more work items than the device
+ *     holds work-groups at once, the work-groups past that first round claim
+ *     the next item at run time (the outputs do not depend on which
+ *     work-group runs an item).  The environment variables
+ *     SPEC_ATTN_FIRST_ROUND (a work-group count >= 1) and SPEC_ATTN_EXTRA_WG
+ *     (surplus work-groups >= 0) override the first round and the surplus;
+ *     they exist for tests.
  *   - When the verify attention cuts a request's KV range into pieces, the
  *     last piece of each (request, KV head, head group) to finish combines
  *     the pieces' partial outputs (bf16 inputs, partial blocks up to 64 KB
