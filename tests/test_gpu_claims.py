@@ -120,3 +120,25 @@ def test_claims_paged_cache(gpu_lib, claims):
     print(f"[case] {name} claimed", flush=True)
     out = _attention(pool, 256, paged=True)["out"]
     assert np.array_equal(out.view(np.uint32), ref.view(np.uint32))
+
+
+@pytest.mark.parametrize("paged", [False, True], ids=["packed", "paged"])
+def test_claims_at_full_size(gpu_lib, claims, monkeypatch, paged):
+    """The 128-request ragged GQA batch at its full size claims by default
+    (more items than the device holds work-groups): its outputs equal the
+    static launch's bit for bit, and both give every request's sampled rows
+    within the oracle's tolerance."""
+    from paper_2505_17074_amd import workload as W
+    pool = W.make_pool(W.CONFIG_BY_NAME["ragged_gqa_b128"], 0)
+    print(f"[case] claims full size ragged_gqa_b128 seed 0 paged {paged} static", flush=True)
+    claims(STATIC, "0")
+    ref = _attention(pool, 0, paged=paged)["out"]
+    print(f"[case] claims full size ragged_gqa_b128 seed 0 paged {paged} default", flush=True)
+    monkeypatch.delenv("SPEC_ATTN_FIRST_ROUND", raising=False)
+    monkeypatch.delenv("SPEC_ATTN_EXTRA_WG", raising=False)
+    out = _attention(pool, 0, paged=paged)["out"]
+    assert np.array_equal(out.view(np.uint32), ref.view(np.uint32))
+    reqs = [0, 1, pool.batch // 2, pool.batch - 1, int(np.argmax(pool.ctx_len))]
+    oracle = U.oracle_attention_rows(pool, reqs)
+    r = U.attention_ratios(out, pool, oracle)
+    assert np.isfinite(r).all() and r.max() <= U.ATTN_RTOL
