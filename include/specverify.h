@@ -73,6 +73,13 @@
  *     attention tolerance, and each choice is deterministic.
  *   - Results are deterministic: the same inputs give bit-identical outputs
  *     (fixed reduction orders, no floating-point atomics).
+ *   - A call captured into a HIP graph may be replayed any number of times,
+ *     also with other calls on the same workspace in between: the tagged
+ *     words are left by each call ready for its own tag again.  A replay
+ *     reads the plan staged at capture, so the staging buffer must keep it
+ *     (for spec_verify_noalloc, whose staging is one static array, no other
+ *     spec_verify_noalloc call with different requests may run between the
+ *     capture and a replay).
  */
 #ifndef SPECVERIFY_H
 #define SPECVERIFY_H

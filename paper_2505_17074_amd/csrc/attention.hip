@@ -552,7 +552,16 @@ void attn_split_mfma(AttnParams p) {
     claim_start(p.claim, p.call_tag, p.first_round, (int)gridDim.x);
   if (idx >= p.first_round) {
     __shared__ int s_item;
-    if (threadIdx.x == 0) s_item = claim_item(p.claim, p.call_tag, p.first_round, (int)gridDim.x);
+    if (threadIdx.x == 0) {
+      s_item = claim_item(p.claim, p.call_tag, p.first_round, (int)gridDim.x);
+      // The last of the grid's claims: every other one has been made, so no
+      // one touches the word again in this call.  Leave it as work-group 0
+      // would start it, so that a replay of this launch with the same tag (a
+      // captured graph) claims from the first round again.
+      if (s_item == (int)gridDim.x - 1)
+        __hip_atomic_store(p.claim, ((unsigned long long)p.call_tag << 32) | (uint32_t)p.first_round,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     __syncthreads();
     idx = __builtin_amdgcn_readfirstlane(s_item);
   }
@@ -781,7 +790,15 @@ void attn_split_mfma(AttnParams p) {
     volatile int* s_last = reinterpret_cast<volatile int*>(lds);
     wait_vm<0>();
     __syncthreads();
-    if (threadIdx.x == 0) *s_last = arrive_last(p.counters + it.stream, p.call_tag, it.nseg) ? 1 : 0;
+    if (threadIdx.x == 0) {
+      const bool last = arrive_last(p.counters + it.stream, p.call_tag, it.nseg);
+      // every piece of the stream has arrived: back to no arrivals under this
+      // tag, so that a replay with the same tag (a captured graph) counts again
+      if (last)
+        __hip_atomic_store(p.counters + it.stream, (unsigned long long)p.call_tag << 32, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      *s_last = last ? 1 : 0;
+    }
     __syncthreads();
     if (!*s_last) return;
     __syncthreads();                  // everyone has read the flag before the combine reuses the LDS
