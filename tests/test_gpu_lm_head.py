@@ -51,7 +51,7 @@ def _check_accept(pool, lmv, got_logits, tag, rule=B.SPEC_TREE_INDEPENDENT):
     unfused = {"accepted_len": b.accepted_len.cpu().numpy(), "next_token": b.next_token.cpu().numpy(),
                "accepted_node": b.accepted_node.cpu().numpy()}
     ref = verify_accept(got_logits, pool.draft_probs, pool.draft_tokens, pool.uniforms, pool.n_q,
-                        dtype=pool.logit_dtype, tree_parent=pool.tree_parent,
+                        dtype=pool.logit_dtype, tree_parent=pool.tree_parent, tree_parents=pool.tree_parents,
                         tree_rule="sequential" if rule == B.SPEC_TREE_SEQUENTIAL else "independent")
     bad, ties = U.compare_accept(fused, ref, pool)
     diff = [i for i in range(pool.batch) if not ref["near_tie"][i] and
@@ -92,6 +92,32 @@ def test_lm_head_accept_against_the_oracle(gpu_lib, name, batch, K, V):
         lmv.acc.tree_rule = B.SPEC_TREE_SEQUENTIAL
         lmv.run()
         _check_accept(pool, lmv, lmv.logits(), name + "/seq", rule=B.SPEC_TREE_SEQUENTIAL)
+
+
+@pytest.mark.parametrize("rule", [B.SPEC_TREE_INDEPENDENT, B.SPEC_TREE_SEQUENTIAL], ids=["independent", "sequential"])
+def test_lm_head_per_request_trees(gpu_lib, rule):
+    """Per-request trees through the LM head (the GEMM copies the node table
+    to the device for the decision): requests alternate between the 15-node
+    binary tree and a 15-node tree of another shape with the same seven
+    nodes that have children (a chain 0..7 with one leaf under each of
+    0..6), so the draft rows keep their layout; fp32 draft probabilities, so
+    every draft token keeps a positive probability under its new parent."""
+    cfg = W.CONFIG_BY_NAME["tree15_b64"]
+    name = f"tree15_b64 per-request trees, rule {rule}"
+    print(f"[case] LM head {name}, batch 8 K 256 V 3000, seed 1", flush=True)
+    pool = W.make_lm_head_pool(cfg, 1, batch=8, hidden_dim=256, vocab=3000)
+    binary = np.asarray(pool.tree_parent, np.int32)
+    other = np.array([-1, 0, 1, 2, 3, 4, 5, 6, 0, 1, 2, 3, 4, 5, 6], np.int32)
+    assert len(binary) == len(other) and set(binary[1:]) == set(other[1:])
+    pool.tree_parents = [binary if i % 2 == 0 else other for i in range(pool.batch)]
+    pool.tree_parent = None
+    lmv = LmHeadVerifier(pool, "cuda")
+    lmv.acc.tree_rule = rule
+    lmv.batch.logits.fill_(float("nan"))
+    lmv.run()
+    got = lmv.logits()
+    _check_logits(pool, got, name)
+    _check_accept(pool, lmv, got, name, rule=rule)
 
 
 def test_lm_head_long_context_vocabulary(gpu_lib):
