@@ -144,3 +144,62 @@ def test_a_replay_without_the_reset_would_skip_items():
     except StopIteration:
         pass
     assert claims == [grid]                               # past the last item: nothing claimed
+
+
+def _arrival(tag, total, lasts):
+    """One piece of a split stream checks in: load, then compare-and-swap
+    (old + 1 under the call's tag, else (tag << 32) | 1); the piece that
+    makes the count `total` is the stream's last and resets the counter to
+    (tag << 32) | 0 for a replay with the same tag."""
+    old = yield ("load",)
+    while True:
+        nw = old + 1 if (old >> 32) == tag else (tag << 32) | 1
+        ok, old2 = yield ("cas", old, nw & MASK64)
+        if ok:
+            break
+        old = old2
+    if (nw & MASK32) == total:
+        yield ("store", tag << 32)
+        lasts.append(1)
+    return None
+
+
+def _run_arrivals(word, tag, total, rng):
+    lasts = []
+    agents = [_arrival(tag, total, lasts) for _ in range(total)]
+    pending = {i: None for i in range(total)}
+    started, live = set(), list(range(total))
+    while live:
+        i = rng.choice(live)
+        try:
+            op = agents[i].send(pending[i]) if i in started else next(agents[i])
+            started.add(i)
+        except StopIteration:
+            live.remove(i)
+            continue
+        if op[0] == "load":
+            pending[i] = word
+        elif op[0] == "cas":
+            if word == op[1]:
+                pending[i] = (True, word)
+                word = op[2]
+            else:
+                pending[i] = (False, word)
+        else:
+            word = op[1]
+    return len(lasts), word
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_split_stream_has_exactly_one_last_piece(seed):
+    """The split combine's arrival counter: whatever the interleaving and the
+    counter's previous contents, exactly one piece is the stream's last, on
+    the call, on a replay with the same tag, and on the next call."""
+    rng = random.Random(1000 + seed)
+    total = rng.randint(1, 48)
+    tag = rng.randint(1, MASK32)
+    word = rng.choice([rng.getrandbits(64), ((tag - 1) & MASK32) << 32 | total, tag << 32])
+    for t in (tag, tag, (tag + 1) & MASK32 or 1):
+        n_last, word = _run_arrivals(word, t, total, rng)
+        assert n_last == 1, (seed, t)
+        assert word == t << 32
