@@ -49,7 +49,7 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("page_tokens", [32, 64, 256])
+@pytest.mark.parametrize("page_tokens", [32, 64, 96, 160, 256])
 @pytest.mark.parametrize("name,kw", CASES, ids=[c[0] for c in CASES])
 def test_paged_equals_packed_bitwise(gpu_lib, name, kw, page_tokens):
     seed = U.case_seed(name)
