@@ -531,7 +531,7 @@ __device__ __forceinline__ void combine_stream(const AttnParams& p, const AttnIt
 // resource based at its page, built from the block table entry (a
 // wave-uniform load, clamped into the pool, issued one ring step ahead of its
 // use); everything else is the packed path's code.
-template <int D, int W, int NS, bool PG>
+template <int D, int W, int NS, int PG>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(WavesPerEu<W>::value)))
 void attn_split_mfma(AttnParams p) {
 #if defined(__HIP_DEVICE_COMPILE__)   // the host pass needs the signature only
@@ -620,8 +620,20 @@ void attn_split_mfma(AttnParams p) {
     const int pg = btr[idx];
     return __builtin_amdgcn_readfirstlane(min(max(pg, 0), p.num_pages - 1));
   };
+  // PG 2: one descriptor per item over this KV head's slice of the pools
+  // (whose byte offsets fit 32 bits); a key at logical position t of page pg
+  // is physical key pg * page_tokens + (t - page start) from the slice's base
+  // (page_bytes = page_tokens * row_bytes)
+  const uint32_t pool_range = PG == 2 ? (uint32_t)(p.pool_bytes - (int64_t)it.kvh * p.kv_sh * 2) : 0u;
+  const __amdgpu_buffer_rsrc_t qk = __builtin_amdgcn_make_buffer_rsrc((void*)Kh, 0, pool_range, 0x00020000);
+  const __amdgpu_buffer_rsrc_t qv = __builtin_amdgcn_make_buffer_rsrc((void*)Vh, 0, pool_range, 0x00020000);
   auto issue = [&](char* stage, auto t, int pg) {
-    if constexpr (PG) {
+    if constexpr (PG == 2) {
+      const int t0 = min(it.kb + 32 * t, last_t0);
+      const int base = t0 - t0 % p.page_tokens;          // the page's first logical key
+      const int pk0 = pg * p.page_tokens;                // the page's first physical key
+      issue_tile<D, W>(stage, qk, qv, row_bytes, pk0 + (t0 - base), pk0 + (it.ke - base), w, lane, X);
+    } else if constexpr (PG == 1) {
       const int t0 = min(it.kb + 32 * t, last_t0);
       const int base = t0 - t0 % p.page_tokens;          // the page's first logical key
       const int64_t pb = (int64_t)pg * p.page_bytes;
@@ -983,7 +995,7 @@ __global__ __launch_bounds__(256) void attn_combine(AttnParams p) {
   for (int x = 0; x < PER; ++x) p.out[((int64_t)qrow * p.Hq + h) * D + lane + 64 * x] = acc[x] * inv;
 }
 
-template <int D, bool PG>
+template <int D, int PG>
 hipError_t launch_mfma(const AttnParams& p, int nr, hipStream_t s) {
   const dim3 grid(p.grid);
   switch (nr) {
@@ -1024,9 +1036,10 @@ int attn_lds_bytes(int D, int nr) {
 
 int attn_resident_per_cu(int D, int nr, int paged) {
   // per (D, waves, paged) build, asked once: the device's own placement
-  static std::atomic<int> cache[2][5][2] = {};
+  static std::atomic<int> cache[2][5][3] = {};
   if ((D != 64 && D != 128) || nr < 1 || nr > 5) return 0;
-  std::atomic<int>& slot = cache[D == 128][nr - 1][paged ? 1 : 0];
+  if (paged < 0 || paged > 2) return 0;
+  std::atomic<int>& slot = cache[D == 128][nr - 1][paged];
   int v = slot.load(std::memory_order_relaxed);
   if (v != 0) return v > 0 ? v : 0;
   auto ask = [](auto kern, int threads) {
@@ -1039,7 +1052,7 @@ int attn_resident_per_cu(int D, int nr, int paged) {
   };
   auto by_build = [&](auto d, auto pg) -> int {
     constexpr int DD = decltype(d)::value;
-    constexpr bool PP = decltype(pg)::value;
+    constexpr int PP = decltype(pg)::value;
     switch (nr) {
       case 1: return ask(attn_split_mfma<DD, 1, SV_NS_W1, PP>, 64);
       case 2: return ask(attn_split_mfma<DD, 2, SV_NS_W2, PP>, 128);
@@ -1050,10 +1063,11 @@ int attn_resident_per_cu(int D, int nr, int paged) {
   };
   using I64 = std::integral_constant<int, 64>;
   using I128 = std::integral_constant<int, 128>;
-  using T = std::true_type;
-  using F = std::false_type;
-  v = D == 64 ? (paged ? by_build(I64{}, T{}) : by_build(I64{}, F{}))
-              : (paged ? by_build(I128{}, T{}) : by_build(I128{}, F{}));
+  using P0 = std::integral_constant<int, 0>;
+  using P1 = std::integral_constant<int, 1>;
+  using P2 = std::integral_constant<int, 2>;
+  v = D == 64 ? (paged == 2 ? by_build(I64{}, P2{}) : paged == 1 ? by_build(I64{}, P1{}) : by_build(I64{}, P0{}))
+              : (paged == 2 ? by_build(I128{}, P2{}) : paged == 1 ? by_build(I128{}, P1{}) : by_build(I128{}, P0{}));
   slot.store(v, std::memory_order_relaxed);
   return v > 0 ? v : 0;
 }
@@ -1062,9 +1076,10 @@ hipError_t launch_attention(const AttnParams& p, int dtype_bf16, int nr_max, hip
   hipError_t e = hipSuccess;
   if (p.n_items > 0) {
     if (dtype_bf16 && p.bt) {
-      e = (p.D == 64) ? launch_mfma<64, true>(p, nr_max, s) : launch_mfma<128, true>(p, nr_max, s);
+      e = p.pool32 ? ((p.D == 64) ? launch_mfma<64, 2>(p, nr_max, s) : launch_mfma<128, 2>(p, nr_max, s))
+                   : ((p.D == 64) ? launch_mfma<64, 1>(p, nr_max, s) : launch_mfma<128, 1>(p, nr_max, s));
     } else if (dtype_bf16) {
-      e = (p.D == 64) ? launch_mfma<64, false>(p, nr_max, s) : launch_mfma<128, false>(p, nr_max, s);
+      e = (p.D == 64) ? launch_mfma<64, 0>(p, nr_max, s) : launch_mfma<128, 0>(p, nr_max, s);
     } else {
       dim3 grid(p.n_items), block(256);
       if (p.D == 64) attn_split_valu<float, 64><<<grid, block, 0, s>>>(p);

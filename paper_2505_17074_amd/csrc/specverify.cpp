@@ -498,7 +498,9 @@ spec_status_t build_plan(const spec_requests_t* r, const spec_attn_args_t* attn,
     // the claim word whenever there are more items than slots, whatever the
     // device reports.
     const int64_t n_it = (int64_t)P.items.size();
-    const int64_t resident = (int64_t)device_cus() * sv::attn_resident_per_cu(D, nr, attn->block_table != nullptr);
+    const int build = !attn->block_table ? 0
+                      : sv::paged_build(attn->num_pages, (int64_t)attn->page_tokens * attn->kv_stride_tok * 2);
+    const int64_t resident = (int64_t)device_cus() * sv::attn_resident_per_cu(D, nr, build);
     const int64_t first = claim_first_round(std::max(slots, resident));
     P.first_round = P.grid = n_it;
     P.claim_word = bf && n_it > std::min(first, slots);
@@ -740,6 +742,8 @@ spec_status_t run(const spec_requests_t* req, const spec_attn_args_t* attn, cons
     a.page_tokens = attn->page_tokens;
     a.num_pages = attn->num_pages;
     a.page_bytes = (int64_t)attn->page_tokens * attn->kv_stride_tok * 2;
+    a.pool_bytes = (int64_t)attn->num_pages * a.page_bytes;
+    a.pool32 = attn->block_table && sv::paged_build(attn->num_pages, a.page_bytes) == 2 ? 1 : 0;
     std::memcpy(a.anc, P.topo.anc, sizeof(a.anc));
     a.nodes = reinterpret_cast<const sv::NodeInfo*>(pl + P.off_nodes);
     a.per_req = P.per_req ? 1 : 0;

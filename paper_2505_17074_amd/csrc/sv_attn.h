@@ -61,6 +61,8 @@ struct AttnParams {
   int32_t page_tokens;
   int32_t num_pages;
   int64_t page_bytes;
+  int64_t pool_bytes;        // num_pages * page_bytes
+  int32_t pool32;            // pool_bytes < 2^32: the paged build with one descriptor per item
   uint32_t anc[kMaxNodes];   // ancestors-or-self masks (kernel arguments: uniform loads)
   // per-request trees (per_req = 1): each request's masks in its node-table
   // entries, read where the host staged them
@@ -91,8 +93,14 @@ int max_rows_per_item(int dtype_bf16, int D);
 hipError_t launch_attention(const AttnParams& p, int dtype_bf16, int nr_max, hipStream_t s);
 // Work-groups of the bf16 split kernel's build for head dim D, nr waves and
 // the paged or packed layout that one compute unit holds at once, as the
-// device reports it; 0 where it cannot be asked (no device).
+// device reports it; 0 where it cannot be asked (no device).  paged: 0 the
+// packed build, 1 the paged build with a descriptor per tile, 2 the paged
+// build with one descriptor per item (pools whose byte offsets fit 32 bits).
 int attn_resident_per_cu(int D, int nr, int paged);
+// The paged build a launch with these pool sizes takes (1 or 2).
+inline int paged_build(int64_t num_pages, int64_t page_bytes) {
+  return num_pages * page_bytes <= (int64_t)0xFFFFFFFF ? 2 : 1;
+}
 // LDS bytes of the bf16 split kernel's build for head dim D and nr row tiles
 // (the fused combine stages its weights there).
 int attn_lds_bytes(int D, int nr);

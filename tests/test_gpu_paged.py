@@ -95,3 +95,30 @@ def test_paged_full_size_bitwise(gpu_lib, idx, page_tokens):
     ref, got, _ = _run(pool, page_tokens, which="attn")
     assert np.array_equal(got["out"].view(np.uint32), ref["out"].view(np.uint32)), cfg.name
     torch.cuda.empty_cache()
+
+
+def test_paged_pool_of_4gib_or_more_equals_packed(gpu_lib):
+    """Pools whose byte offsets do not fit 32 bits take the paged build with a
+    buffer descriptor per tile; pools that fit take one descriptor per item
+    over the pool.  A pool of just over 4 GiB per K and V (the pages the
+    batch uses scattered among the spare ones) gives the packed outputs bit
+    for bit, as the small pools above do."""
+    name = "paged_large_pool"
+    seed = U.case_seed(name)
+    pool = U.custom_pool(ctx=[300, 1200, 40, 5000], k=[5, 7, 3, 7], Hq=8, Hkv=2, seed=seed)
+    b = DeviceBatch(pool, "cuda")
+    packed = Verifier(b)
+    packed.run("attn")
+    ref = packed.results()["out"]
+    P = 64
+    page_bytes = P * b.k.stride(0) * 2
+    spare = (1 << 32) // page_bytes + 8                  # num_pages * page_bytes > 2^32
+    print(f"[case] {name} seed {seed} page_tokens {P} spare pages {spare} "
+          f"pool {(spare + 200) * page_bytes / 2**30:.2f} GiB per K and V", flush=True)
+    pk = PagedKV(b, P, seed=seed, spare=spare)
+    assert pk.num_pages * page_bytes > (1 << 32)
+    b.out.fill_(float("nan"))
+    paged = Verifier(b, attn=pk.attn_args(0))
+    paged.run("attn")
+    got = paged.results()["out"]
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
